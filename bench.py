@@ -1,0 +1,195 @@
+"""Benchmark of one segment re-prefill step on one MI355X.
+
+Workload (Llama-3-8B-shaped attention layer): 32 query heads, 8 KV heads,
+head_dim 128, bf16, page size 16.  A cached context of 683 pages (10928
+tokens) is spliced by dropping a contiguous run of 171 pages (25%), leaving an
+8192-token prefix; a 2048-token transformed segment is appended after it and
+its causal grouped-query attention is computed over prefix + segment.
+
+One step = sa_kv_assemble -> sa_kv_append -> sa_segment_prefill_attn, all on
+the current stream with inputs resident in HBM.  Every step uses one of R
+disjoint copies of the cache (default 8 x 128 MB per pool), so the 256 MB
+Infinity Cache cannot hold the data a step reads from its previous use.
+
+Prints one JSON line.  `value` is segment tokens per second over whole steps;
+per-kernel averages come from HIP events recorded on the launch stream around
+every call inside the timed region.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+sys.path.insert(0, os.path.join(ROOT, "tests"))
+
+PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA: 256 CU x 4096 flop/clk x 2.4 GHz
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--rotate", type=int, default=8, help="disjoint cache copies cycled per step")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-stride", type=int, default=16, help="oracle sample: every n-th token")
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+    import paper_2607_00151_amd as sa
+    if not os.path.exists(sa.library_path()):
+        from paper_2607_00151_amd import build
+        build.build()
+    import workloads
+    from harness import dev_i32, dev_u16, new_pool, place_range
+    from workloads.configs import source_rows
+
+    w = workloads.make("c2")
+    a = w.asm
+    R = max(1, args.rotate)
+    base_slots = w.num_slots
+    L = sa.Layout(num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads, head_dim=128,
+                  page_size=w.page_size, num_layers=1, num_slots=base_slots * R)
+
+    class Big:   # the workload seen through a pool R times larger
+        num_slots = base_slots * R
+        num_kv_heads = w.num_kv_heads
+        page_size = w.page_size
+        head_dim = 128
+    kp, vp = new_pool(Big), new_pool(Big)
+    copies = []
+    for r in range(R):
+        off = r * base_slots
+        src_ix = a.src_indices + off
+        for pool, which in ((kp, "k"), (vp, "v")):
+            place_range(pool, 0, w, lambda b, which=which: source_rows(w, b, which), a.src_indptr,
+                        src_ix, a.src_len)
+        copies.append(dict(sip=dev_i32(a.src_indptr), sid=dev_i32(src_ix), fresh=dev_i32(a.fresh + off),
+                           dip=torch.zeros(w.batch + 1, dtype=torch.int32, device="cuda"),
+                           did=torch.zeros(len(a.fresh), dtype=torch.int32, device="cuda")))
+    q = dev_u16(w.q)
+    ks, vs = dev_u16(w.k_seg()), dev_u16(w.v_seg())
+    T = int(w.qlen.sum())
+    o = torch.empty((T, w.num_q_heads, 128), dtype=torch.int16, device="cuda")
+    lse = torch.empty((T, w.num_q_heads), dtype=torch.float32, device="cuda")
+    ctx = sa.Context(0)
+    stream = torch.cuda.current_stream()
+
+    def step(r, ev=None):
+        c = copies[r % R]
+        if ev is not None:
+            ev[0].record(stream)
+        kept = sa.sa_kv_assemble(ctx, L, kp, vp, kp, vp, a.src_len, a.keep_indptr, a.keep_spans,
+                                 a.reserve, c["sip"], c["sid"], c["fresh"], c["dip"], c["did"])
+        if ev is not None:
+            ev[1].record(stream)
+        sa.sa_kv_append(ctx, L, 0, kp, vp, ks, vs, kept, w.qlen, c["dip"], c["did"])
+        if ev is not None:
+            ev[2].record(stream)
+        sa.sa_segment_prefill_attn(ctx, L, 0, q, kp, vp, w.qlen, kept + w.qlen, c["dip"], c["did"],
+                                   w.scale, o, lse)
+        if ev is not None:
+            ev[3].record(stream)
+        return kept
+
+    for i in range(args.warmup):
+        step(i)
+    sa.sa_sync_check(ctx)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(K):
+        step(args.warmup + i, evs[i])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    sa.sa_sync_check(ctx)
+    total_ms = t_start.elapsed_time(t_end)
+    asm_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    app_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    attn_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    ms_per_step = total_ms / K
+
+    Hkv, P, D = w.num_kv_heads, w.page_size, 128
+    page_bytes = 2 * Hkv * P * D * 2                      # K and V of one slot
+    kept_pages = int(sum(e - b for b, e in a.keep_spans))
+    n_dst = int(sum(-(-int(x + y) // P) for x, y in zip(w.pre, w.qlen)))
+    asm_bytes = 2 * kept_pages * page_bytes + 4 * (n_dst + kept_pages + w.batch + 1)
+    app_bytes = 2 * T * Hkv * D * 2 * 2                   # K and V rows, read + write
+    flops = w.attn_flops()
+    attn_tflops = flops / (attn_ms * 1e-3) / 1e12
+
+    rec = {
+        "metric": "segment-prefill tokens/s + attn TFLOP/s (% MFMA peak); KV assemble GB/s (% HBM)",
+        "value": T / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "segment re-prefill, Llama-3-8B-shaped layer: Hq 32 / Hkv 8 / d 128, "
+                        "page 16; splice 683 -> 512 pages (drop 171), append 2048-token segment, "
+                        "causal GQA over 8192 + 2048",
+            "batch": 1, "prefix": int(w.pre[0]), "segment": T, "page_size": P,
+            "cache_copies_rotated": R,
+        },
+        "attn": {"ms": attn_ms, "gflop": flops / 1e9, "tflops": attn_tflops,
+                 "frac_of_bf16_peak": attn_tflops / PEAK_BF16_TFLOPS,
+                 "tokens_per_s": T / (attn_ms * 1e-3)},
+        "assemble": {"ms": asm_ms, "bytes": asm_bytes, "gbs": asm_bytes / (asm_ms * 1e-3) / 1e9,
+                     "frac_of_hbm": asm_bytes / (asm_ms * 1e-3) / 1e9 / PEAK_HBM_GBS},
+        "append": {"ms": app_ms, "bytes": app_bytes, "gbs": app_bytes / (app_ms * 1e-3) / 1e9},
+        "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": attn_tflops / PEAK_BF16_TFLOPS, "traffic": None},
+        "paper_context": "paper reports up to 11.9x transform-point TTFT reduction end to end on "
+                         "H100 80GB (SGLang, Qwen3-8B); no kernel-level numbers",
+    }
+
+    if not args.no_cpu_baseline:
+        import oracle
+        stride = max(1, args.cpu_stride)
+        toks = np.arange(0, T, stride, dtype=np.int64)
+        tok_rows = np.repeat(toks, w.num_q_heads)
+        heads = np.tile(np.arange(w.num_q_heads, dtype=np.int32), len(toks))
+        t0 = time.perf_counter()
+        oracle.attention_rows(w.q, w.k, w.v, w.q_indptr, w.kv_indptr, w.num_q_heads,
+                              w.num_kv_heads, w.scale, tok_rows, heads)
+        dt = time.perf_counter() - t0
+        rec["cpu_baseline"] = {
+            "value": len(toks) / dt, "unit": "tokens/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"attention of every {stride}th segment token ({len(toks)} tokens x "
+                      f"{w.num_q_heads} heads) of the same workload; {dt:.2f} s",
+        }
+    ctx.close()
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,198 @@
+/*
+ * sa.h — C ABI of the segment re-prefill library (MI355X / gfx950).
+ *
+ * The library implements the data-parallel work behind lookahead context
+ * engineering (SmoothAgent, arXiv 2607.00151): a context transformation
+ * invalidates the KV cache and forces a re-prefill (paper Sec. 1, Sec. 3.1);
+ * the lookahead stream builds the transformed segment's KV on top of the
+ * already transformed prefix, in order (Sec. 3.2); at commit the transformed
+ * prefix is spliced in place of the old one (Sec. 3.2, Listing of the agent
+ * loop); keep-recent-K keeps the head of the context and its recent turns and
+ * drops the run in between (Sec. 3.4).  The three data operations are:
+ *
+ *   sa_kv_assemble           commit splice: gather the surviving pages of a
+ *                            cached context into fresh slots, in order, and
+ *                            reserve room for the segment that follows
+ *   sa_kv_append             write a new segment's K/V rows into the cache
+ *   sa_segment_prefill_attn  causal grouped-query attention of the segment's
+ *                            queries over the cached prefix plus, causally,
+ *                            the segment itself (Sec. 4, prefill-attention
+ *                            term: segment token i sees prefix + i + 1 keys)
+ *
+ * Data layout (all device memory is owned by the caller):
+ *   bf16 values are IEEE bfloat16 bit patterns (uint16).
+ *   K pool, V pool  bf16 [num_layers][num_slots][num_kv_heads][page_size][head_dim]
+ *                   (one slot holds page_size consecutive tokens of every KV head
+ *                   of one layer; a slot id is the same in every layer)
+ *   page table      CSR over sequences: the pages of sequence b are
+ *                   indices[indptr[b] .. indptr[b+1]-1], logical token x of b is
+ *                   row x % page_size of slot indices[indptr[b] + x / page_size]
+ *   Q, O            bf16 [sum q_len][num_q_heads][head_dim], sequences back to back
+ *   new K, V rows   bf16 [sum new_len][num_kv_heads][head_dim]
+ *   LSE             fp32 [sum q_len][num_q_heads], natural log of the softmax
+ *                   denominator of the scaled scores
+ * Query head h reads KV head h / (num_q_heads / num_kv_heads).
+ *
+ * Conventions:
+ *   - Lengths, spans and counts are small HOST int32 arrays, so grids are
+ *     sized without a device round trip; page tables and free lists live on
+ *     the device.
+ *   - Every call validates its arguments on the host before touching HIP and
+ *     returns a status; nothing throws across the ABI.  Validation order:
+ *     layout and shapes, then pointers, then the context.
+ *   - Calls enqueue work on `stream` (a hipStream_t; NULL is the default
+ *     stream) and return without synchronising.  Buffers must stay valid until
+ *     the stream has run the work.
+ *   - A context keeps per-call plans (work lists) in device memory and reuses
+ *     an uploaded plan when the next call of the same kind needs the same one.
+ *     Calls on one context must therefore be ordered: use one stream per
+ *     context (or one context per stream / thread).
+ *   - Page ids inside device tables are range-checked by the kernels: a page
+ *     beyond a sequence's list or a slot outside [0, num_slots) is skipped
+ *     (never dereferenced) and latched in a device flag that sa_sync_check
+ *     reports.  Reads of such pages contribute zeros.
+ *   - Pointers to pools, Q, O, K/V rows must be 16-byte aligned.
+ */
+#ifndef SA_H
+#define SA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum sa_status {
+    SA_OK = 0,
+    SA_ERR_NULL = 1,          /* a required pointer (or the context) is NULL            */
+    SA_ERR_SHAPE = 2,         /* inconsistent sizes or lengths                          */
+    SA_ERR_UNSUPPORTED = 3,   /* head_dim != 128, page_size not 16 or 32, ...          */
+    SA_ERR_ALIGN = 4,         /* a data pointer is not 16-byte aligned                  */
+    SA_ERR_RANGE = 5,         /* a span or page id is out of range                      */
+    SA_ERR_NO_PAGES = 6,      /* free list or destination table too small               */
+    SA_ERR_HIP = 7,           /* a HIP runtime call failed (see sa_last_error)          */
+    SA_ERR_DEVICE = 8         /* no usable gfx950 device                                 */
+} sa_status;
+
+typedef struct sa_ctx sa_ctx;
+
+/* Cache geometry shared by every call that touches the pools. */
+typedef struct sa_layout {
+    int32_t num_q_heads;      /* Hq, a multiple of num_kv_heads                         */
+    int32_t num_kv_heads;     /* Hkv >= 1                                               */
+    int32_t head_dim;         /* must be 128                                            */
+    int32_t page_size;        /* tokens per slot: 16 or 32                              */
+    int32_t num_layers;       /* layers held by each pool (>= 1)                        */
+    int64_t num_slots;        /* slots per layer                                        */
+} sa_layout;
+
+/* Device page table in CSR form (see the layout notes above). */
+typedef struct sa_pages {
+    const int32_t *indptr;    /* device [batch + 1]                                     */
+    const int32_t *indices;   /* device [indptr[batch]] slot ids                        */
+} sa_pages;
+
+/* Create a context on HIP device `device` (must be gfx950).  The context owns
+ * only plan buffers, pinned staging, split-KV scratch and an error flag.
+ * Returns SA_ERR_DEVICE if the device is missing or not gfx950. */
+sa_status sa_create(int device, sa_ctx **out);
+
+/* Release a context (waits for the device first).  NULL is ignored. */
+void sa_destroy(sa_ctx *ctx);
+
+/* Static description of a status code. */
+const char *sa_status_string(sa_status status);
+
+/* Message of the most recent failing call on this thread ("" if none). */
+const char *sa_last_error(void);
+
+/* Wait for `stream`, then report SA_ERR_RANGE if any kernel of this context
+ * met an out-of-range page id or slot since the last check (and clear it). */
+sa_status sa_sync_check(sa_ctx *ctx, void *stream);
+
+/*
+ * sa_kv_append — store a segment's new K/V rows in the cache (paper Sec. 3.2:
+ * the lookahead transform builds KV on the transformed prefix).
+ *
+ * For each sequence b, new token t (0 <= t < h_new_len[b]) goes to logical
+ * position h_start[b] + t of layer `layer`: slot
+ * pages.indices[pages.indptr[b] + (h_start[b] + t) / page_size], row
+ * (h_start[b] + t) % page_size.  Rows are copied bit for bit; nothing else in
+ * the pools changes.  k_new / v_new hold the rows of all sequences back to
+ * back ([sum new_len][Hkv][128]).  A sequence with h_new_len[b] == 0 is a
+ * no-op.  The page list of b must cover the written positions.
+ *
+ * Errors: SA_ERR_SHAPE (batch < 1, negative start or length, layer outside
+ * [0, num_layers)), SA_ERR_UNSUPPORTED, SA_ERR_NULL, SA_ERR_ALIGN, SA_ERR_HIP.
+ */
+sa_status sa_kv_append(sa_ctx *ctx, const sa_layout *layout, int32_t layer,
+                       void *k_pool, void *v_pool,
+                       const void *k_new, const void *v_new,
+                       int32_t batch, const int32_t *h_start, const int32_t *h_new_len,
+                       sa_pages pages, void *stream);
+
+/*
+ * sa_kv_assemble — commit splice into a replacement cache (paper Sec. 3.2
+ * commit; Sec. 3.4 keep-recent-K drops an interior run of turns).
+ *
+ * Sequence b's source cache holds h_src_len[b] tokens on the pages of `src`.
+ * Its surviving pages are the [begin, end) logical page spans
+ * h_keep_spans[2*s], h_keep_spans[2*s+1] for s in h_keep_indptr[b] ..
+ * h_keep_indptr[b+1]-1 (ascending, disjoint, non-empty, within the source
+ * pages).  The replacement cache of b is those pages in order, renumbered
+ * from 0, followed by enough new pages for h_reserve[b] more tokens:
+ *   kept_b  = tokens on the surviving pages   (returned in h_dst_len[b])
+ *   pages_b = ceil((kept_b + h_reserve[b]) / page_size)
+ * Destination slots are taken from the front of the device free list
+ * d_fresh[0 .. num_fresh), sequence after sequence.  Every surviving page is
+ * copied whole (all page_size rows, every KV head, every layer) from its
+ * source slot to its destination slot; reserved pages are left untouched.
+ * The destination page table is written to d_dst_indptr[batch + 1] and
+ * d_dst_indices[sum pages_b] (capacity dst_capacity entries).
+ *
+ * k_dst / v_dst may be the same pools as k_src / v_src.  Fresh slots must not
+ * be surviving source slots of this call (the copy reads and writes in
+ * parallel); nothing checks this on the hot path.
+ *
+ * Errors: SA_ERR_SHAPE, SA_ERR_RANGE (bad span), SA_ERR_NO_PAGES (free list
+ * or dst_capacity too small), SA_ERR_UNSUPPORTED, SA_ERR_NULL, SA_ERR_ALIGN,
+ * SA_ERR_HIP.
+ */
+sa_status sa_kv_assemble(sa_ctx *ctx, const sa_layout *layout,
+                         const void *k_src, const void *v_src, void *k_dst, void *v_dst,
+                         int32_t batch, const int32_t *h_src_len,
+                         const int32_t *h_keep_indptr, const int32_t *h_keep_spans,
+                         const int32_t *h_reserve,
+                         sa_pages src, const int32_t *d_fresh, int32_t num_fresh,
+                         int32_t *d_dst_indptr, int32_t *d_dst_indices, int32_t dst_capacity,
+                         int32_t *h_dst_len, void *stream);
+
+/*
+ * sa_segment_prefill_attn — causal grouped-query attention of each
+ * sequence's last h_q_len[b] tokens over its h_kv_len[b] cached tokens
+ * (paper Sec. 4, prefill-attention term; decode rows are the q_len = 1 case of
+ * the decode-attention term).
+ *
+ * With prefix_b = h_kv_len[b] - h_q_len[b], segment row i of query head h
+ * attends keys 0 .. prefix_b + i of KV head h / (Hq / Hkv) in layer `layer`:
+ *   O = softmax(softmax_scale * q . K^T) V,   LSE = log(sum exp(scale * q . k))
+ * The segment's own K/V must already be in the cache (sa_kv_append).  Output
+ * rows are bf16 (round to nearest even); `lse` may be NULL.  Sequences with
+ * h_q_len[b] == 0 are skipped.  Arithmetic: bf16 MFMA products with fp32
+ * accumulation, fp32 online softmax, probabilities rounded to bf16 before the
+ * PV product.
+ *
+ * Errors: SA_ERR_SHAPE (0 <= q_len <= kv_len violated, bad batch or layer),
+ * SA_ERR_UNSUPPORTED, SA_ERR_NULL, SA_ERR_ALIGN, SA_ERR_HIP.
+ */
+sa_status sa_segment_prefill_attn(sa_ctx *ctx, const sa_layout *layout, int32_t layer,
+                                  const void *q, const void *k_pool, const void *v_pool,
+                                  int32_t batch, const int32_t *h_q_len, const int32_t *h_kv_len,
+                                  sa_pages pages, float softmax_scale,
+                                  void *o, float *lse, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SA_H */

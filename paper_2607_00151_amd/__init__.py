@@ -1,0 +1,203 @@
+"""MI355X-native segment re-prefill: Python binding of the C ABI in include/sa.h.
+
+The binding only marshals arguments: torch tensors supply device pointers and
+the current HIP stream, host length arrays are converted to int32, and every
+computation happens in the HIP kernels of ``libsa.so``.  If the library is not
+built, importing works but every call raises -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+__all__ = [
+    "Layout", "Context", "SaError", "library_path", "load_library",
+    "sa_kv_append", "sa_kv_assemble", "sa_segment_prefill_attn", "sa_sync_check",
+    "EXPORTED_SYMBOLS",
+]
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_PKG, "libsa.so")
+_lib = None
+
+EXPORTED_SYMBOLS = ("sa_create", "sa_destroy", "sa_status_string", "sa_last_error",
+                    "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_segment_prefill_attn")
+
+STATUS = {0: "SA_OK", 1: "SA_ERR_NULL", 2: "SA_ERR_SHAPE", 3: "SA_ERR_UNSUPPORTED",
+          4: "SA_ERR_ALIGN", 5: "SA_ERR_RANGE", 6: "SA_ERR_NO_PAGES", 7: "SA_ERR_HIP",
+          8: "SA_ERR_DEVICE"}
+
+
+class SaError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+        self.name = STATUS.get(status, str(status))
+
+
+class Layout(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("num_layers", ctypes.c_int32), ("num_slots", ctypes.c_int64)]
+
+
+class _Pages(ctypes.Structure):
+    _fields_ = [("indptr", ctypes.c_void_p), ("indices", ctypes.c_void_p)]
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load_library():
+    """Load libsa.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(f"{_LIB_PATH} is not built; run paper_2607_00151_amd.build.build()")
+    lib = ctypes.CDLL(_LIB_PATH)
+    P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    LP = ctypes.POINTER(Layout)
+    lib.sa_create.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_void_p)]
+    lib.sa_destroy.argtypes = [P]
+    lib.sa_destroy.restype = None
+    lib.sa_status_string.argtypes = [ctypes.c_int]
+    lib.sa_status_string.restype = ctypes.c_char_p
+    lib.sa_last_error.argtypes = []
+    lib.sa_last_error.restype = ctypes.c_char_p
+    lib.sa_sync_check.argtypes = [P, P]
+    lib.sa_kv_append.argtypes = [P, LP, I32, P, P, P, P, I32, P, P, _Pages, P]
+    lib.sa_kv_assemble.argtypes = [P, LP, P, P, P, P, I32, P, P, P, P, _Pages, P, I32, P, P, I32,
+                                   P, P]
+    lib.sa_segment_prefill_attn.argtypes = [P, LP, I32, P, P, P, I32, P, P, _Pages, ctypes.c_float,
+                                            P, P, P]
+    for name in ("sa_create", "sa_sync_check", "sa_kv_append", "sa_kv_assemble",
+                 "sa_segment_prefill_attn"):
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != 0:
+        msg = load_library().sa_last_error().decode(errors="replace")
+        raise SaError(status, msg)
+
+
+def _ptr(t):
+    """Device (or host) address of a tensor / array, or None."""
+    if t is None:
+        return None
+    if hasattr(t, "data_ptr"):
+        return t.data_ptr() or None
+    if isinstance(t, int):
+        return t or None
+    return t.ctypes.data
+
+
+def _host_i32(x):
+    a = np.ascontiguousarray(np.asarray(x, dtype=np.int64))
+    if a.size and (a.min() < -2**31 or a.max() >= 2**31):
+        raise OverflowError("value does not fit int32")
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if hasattr(stream, "cuda_stream"):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _pages(indptr, indices):
+    return _Pages(_ptr(indptr), _ptr(indices))
+
+
+class Context:
+    """Owns an sa_ctx (plan buffers, staging, split scratch) on one device."""
+
+    def __init__(self, device: int = 0):
+        lib = load_library()
+        h = ctypes.c_void_p()
+        _check(lib.sa_create(int(device), ctypes.byref(h)))
+        self._h = h
+        self.device = device
+
+    @property
+    def handle(self):
+        return self._h
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            load_library().sa_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+def _ctx_handle(ctx):
+    if ctx is None:
+        return None
+    return ctx.handle if isinstance(ctx, Context) else ctx
+
+
+def sa_sync_check(ctx, stream=None):
+    _check(load_library().sa_sync_check(_ctx_handle(ctx), _stream(stream)))
+
+
+def sa_kv_append(ctx, layout: Layout, layer: int, k_pool, v_pool, k_new, v_new, start, new_len,
+                 pages_indptr, pages_indices, stream=None):
+    start, new_len = _host_i32(start), _host_i32(new_len)
+    if start.shape != new_len.shape:
+        raise ValueError("start and new_len differ in length")
+    _check(load_library().sa_kv_append(
+        _ctx_handle(ctx), ctypes.byref(layout), int(layer), _ptr(k_pool), _ptr(v_pool),
+        _ptr(k_new), _ptr(v_new), int(len(new_len)), _ptr(start), _ptr(new_len),
+        _pages(pages_indptr, pages_indices), _stream(stream)))
+
+
+def sa_kv_assemble(ctx, layout: Layout, k_src, v_src, k_dst, v_dst, src_len, keep_indptr,
+                   keep_spans, reserve, src_indptr, src_indices, fresh, dst_indptr, dst_indices,
+                   stream=None):
+    """Returns the kept token count of every sequence (numpy int32)."""
+    src_len, reserve = _host_i32(src_len), _host_i32(reserve)
+    keep_indptr = _host_i32(keep_indptr)
+    keep_spans = _host_i32(np.asarray(keep_spans).reshape(-1))
+    B = len(src_len)
+    if len(reserve) != B or len(keep_indptr) != B + 1:
+        raise ValueError("per-sequence arrays disagree on the batch size")
+    dst_len = np.zeros(B, dtype=np.int32)
+    _check(load_library().sa_kv_assemble(
+        _ctx_handle(ctx), ctypes.byref(layout), _ptr(k_src), _ptr(v_src), _ptr(k_dst), _ptr(v_dst),
+        B, _ptr(src_len), _ptr(keep_indptr), _ptr(keep_spans) if keep_spans.size else None,
+        _ptr(reserve), _pages(src_indptr, src_indices), _ptr(fresh), int(fresh.numel()),
+        _ptr(dst_indptr), _ptr(dst_indices), int(dst_indices.numel()), _ptr(dst_len),
+        _stream(stream)))
+    return dst_len
+
+
+def sa_segment_prefill_attn(ctx, layout: Layout, layer: int, q, k_pool, v_pool, q_len, kv_len,
+                            pages_indptr, pages_indices, softmax_scale: float, o, lse=None,
+                            stream=None):
+    q_len, kv_len = _host_i32(q_len), _host_i32(kv_len)
+    if q_len.shape != kv_len.shape:
+        raise ValueError("q_len and kv_len differ in length")
+    _check(load_library().sa_segment_prefill_attn(
+        _ctx_handle(ctx), ctypes.byref(layout), int(layer), _ptr(q), _ptr(k_pool), _ptr(v_pool),
+        int(len(q_len)), _ptr(q_len), _ptr(kv_len), _pages(pages_indptr, pages_indices),
+        float(softmax_scale), _ptr(o), _ptr(lse), _stream(stream)))

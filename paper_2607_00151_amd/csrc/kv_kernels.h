@@ -1,0 +1,156 @@
+// Bandwidth-bound page kernels: segment append (scatter) and commit-splice
+// assembly (whole-page gather into fresh slots).  Both move 16-byte chunks
+// with every lane of a wave on consecutive addresses, and range-check every
+// page id before touching memory.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace sa {
+
+// ---------------------------------------------------------------- append
+
+struct AppendArgs {
+  uint16_t* k_pool;          // offset to the layer
+  uint16_t* v_pool;
+  const uint16_t* k_new;     // [sum new][Hkv][128]
+  const uint16_t* v_new;
+  const int32_t* tok_begin;  // [B + 1] first new token of each sequence
+  const int32_t* start;      // [B] logical position of each sequence's first new token
+  const int32_t* indptr;
+  const int32_t* indices;
+  int32_t* err;
+  int64_t num_slots;
+  int64_t total_chunks;      // sum new * Hkv * 16
+  int32_t B, Hkv, P;
+};
+
+// Largest b with tok_begin[b] <= t (tok_begin is non-decreasing).
+__device__ __forceinline__ int find_seq(const int32_t* tok_begin, int B, int t) {
+  int lo = 0, hi = B - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (tok_begin[mid] <= t) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+constexpr int kAppendChunksPerThread = 4;
+
+__global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
+  const int per_tok = a.Hkv * 16;
+#pragma unroll
+  for (int u = 0; u < kAppendChunksPerThread; ++u) {
+    const int64_t c = ((int64_t)blockIdx.x * kAppendChunksPerThread + u) * 256 + threadIdx.x;
+    if (c >= a.total_chunks) return;
+    const int t = (int)(c / per_tok);
+    const int rem = (int)(c - (int64_t)t * per_tok);
+    const int g = rem >> 4, ch = rem & 15;
+    const int b = find_seq(a.tok_begin, a.B, t);
+    const int x = a.start[b] + (t - a.tok_begin[b]);
+    const int page = x / a.P, row = x - page * a.P;
+    const int32_t base = a.indptr[b];
+    if (page >= a.indptr[b + 1] - base) { atomicOr(a.err, 2); continue; }
+    const int32_t slot = a.indices[base + page];
+    if (slot < 0 || (int64_t)slot >= a.num_slots) { atomicOr(a.err, 2); continue; }
+    const int64_t dst = (((int64_t)slot * a.Hkv + g) * a.P + row) * 128 + ch * 8;
+    const u32x4 kx = ld_u32x4(a.k_new + c * 8);
+    const u32x4 vx = ld_u32x4(a.v_new + c * 8);
+    st_u32x4(a.k_pool + dst, kx);
+    st_u32x4(a.v_pool + dst, vx);
+  }
+}
+
+// ---------------------------------------------------------------- assemble
+
+struct AsmSpan {
+  int32_t seq;
+  int32_t src_page;     // first logical source page of the span
+  int32_t dst_page;     // its logical page in the replacement cache
+  int32_t first_unit;   // index of the span's first page among all copied pages
+};
+
+struct AsmArgs {
+  const uint16_t* k_src;
+  const uint16_t* v_src;
+  uint16_t* k_dst;
+  uint16_t* v_dst;
+  const AsmSpan* spans;        // [n_spans], first_unit ascending
+  const int32_t* dst_indptr;   // [B + 1] plan copy of the destination table offsets
+  const int32_t* src_indptr;
+  const int32_t* src_indices;
+  const int32_t* fresh;
+  int32_t* out_indptr;         // [B + 1]
+  int32_t* out_indices;        // [n_dst]
+  int32_t* err;
+  int64_t num_slots;
+  int64_t slot_elems;          // Hkv * P * 128
+  int64_t layer_elems;         // num_slots * slot_elems
+  int32_t n_spans, n_units, n_dst, B;
+};
+
+// grid: x = max(units, table blocks), y = layer.  One block copies one page of
+// one layer: slot_elems * 2 bytes of K and as many of V.
+__global__ __launch_bounds__(256) void assemble_kernel(AsmArgs a) {
+  const int u = blockIdx.x;
+  const int layer = blockIdx.y;
+  const int tid = threadIdx.x;
+
+  // the destination table (layer 0 blocks write disjoint slices of it)
+  if (layer == 0) {
+    const int idx = u * 256 + tid;
+    if (idx < a.n_dst) a.out_indices[idx] = a.fresh[idx];
+    if (idx <= a.B) a.out_indptr[idx] = a.dst_indptr[idx];
+  }
+  if (u >= a.n_units) return;
+
+  // span holding unit u
+  int lo = 0, hi = a.n_spans - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.spans[mid].first_unit <= u) lo = mid; else hi = mid - 1;
+  }
+  const AsmSpan sp = a.spans[lo];
+  const int off = u - sp.first_unit;
+  const int sp_page = sp.src_page + off;
+  const int dp_page = sp.dst_page + off;
+  const int32_t sbase = a.src_indptr[sp.seq];
+  if (sp_page >= a.src_indptr[sp.seq + 1] - sbase) { if (tid == 0) atomicOr(a.err, 4); return; }
+  const int32_t s_slot = a.src_indices[sbase + sp_page];
+  const int32_t d_slot = a.fresh[a.dst_indptr[sp.seq] + dp_page];
+  if (s_slot < 0 || (int64_t)s_slot >= a.num_slots || d_slot < 0 || (int64_t)d_slot >= a.num_slots) {
+    if (tid == 0) atomicOr(a.err, 4);
+    return;
+  }
+  const int64_t lo_off = (int64_t)layer * a.layer_elems;
+  const uint16_t* ks = a.k_src + lo_off + (int64_t)s_slot * a.slot_elems;
+  const uint16_t* vs = a.v_src + lo_off + (int64_t)s_slot * a.slot_elems;
+  uint16_t* kd = a.k_dst + lo_off + (int64_t)d_slot * a.slot_elems;
+  uint16_t* vd = a.v_dst + lo_off + (int64_t)d_slot * a.slot_elems;
+  const int n_chunks = (int)(a.slot_elems / 8);
+  // 8 chunks in flight per thread per pass (K and V)
+  for (int base = 0; base < n_chunks; base += 256 * 4) {
+    u32x4 kx[4], vx[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c = base + j * 256 + tid;
+      if (c < n_chunks) {
+        kx[j] = ld_u32x4(ks + c * 8);
+        vx[j] = ld_u32x4(vs + c * 8);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c = base + j * 256 + tid;
+      if (c < n_chunks) {
+        st_u32x4(kd + c * 8, kx[j]);
+        st_u32x4(vd + c * 8, vx[j]);
+      }
+    }
+  }
+}
+
+}  // namespace sa

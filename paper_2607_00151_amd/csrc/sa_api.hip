@@ -1,0 +1,559 @@
+// Host side of the C ABI declared in include/sa.h: argument validation, work
+// planning, plan upload and kernel launches.  Every entry point validates on
+// the host before its first HIP call.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "sa.h"
+#include "attn_kernel.h"
+#include "kv_kernels.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+sa_status fail(sa_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+#define SA_HIP(call)                                                                 \
+  do {                                                                               \
+    hipError_t e_ = (call);                                                          \
+    if (e_ != hipSuccess)                                                            \
+      return fail(SA_ERR_HIP, "%s failed: %s", #call, hipGetErrorString(e_));        \
+  } while (0)
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr int kNumXcd = 8;         // MI355X: 8 accelerator complex dies, 32 CUs each
+constexpr int kRing = 8;           // pinned staging buffers in flight
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Byte image of a plan: sub-arrays at 256-byte aligned offsets.
+struct PlanImage {
+  std::vector<uint8_t> bytes;
+  template <class T>
+  size_t add(const T* data, size_t n) {
+    size_t off = align_up(bytes.size(), 256);
+    bytes.resize(off + sizeof(T) * n);
+    if (n) memcpy(bytes.data() + off, data, sizeof(T) * n);
+    return off;
+  }
+};
+
+enum PlanKind { kPlanAppend = 0, kPlanAssemble = 1, kPlanAttn = 2, kPlanKinds = 3 };
+
+}  // namespace
+
+struct sa_ctx {
+  int device = 0;
+  int num_cu = 256;
+  int32_t* d_err = nullptr;
+  struct DevPlan {
+    uint8_t* dev = nullptr;
+    size_t cap = 0;
+    std::vector<uint8_t> shadow;   // what the device buffer holds
+    void* stream = nullptr;        // stream that last wrote it
+    bool valid = false;
+  } plans[kPlanKinds];
+  struct Stage {
+    void* host = nullptr;
+    size_t cap = 0;
+    hipEvent_t ev = nullptr;
+    bool pending = false;
+  } ring[kRing];
+  int ring_next = 0;
+  float* part = nullptr;           // split-KV partials
+  size_t part_cap = 0;             // bytes
+};
+
+namespace {
+
+// Make the device copy of a plan current; returns its device address.
+sa_status upload_plan(sa_ctx* ctx, PlanKind kind, const PlanImage& img, hipStream_t stream,
+                      uint8_t** dev) {
+  sa_ctx::DevPlan& dp = ctx->plans[kind];
+  const size_t n = img.bytes.size();
+  if (dp.valid && dp.stream == (void*)stream && dp.shadow.size() == n &&
+      memcmp(dp.shadow.data(), img.bytes.data(), n) == 0) {
+    *dev = dp.dev;
+    return SA_OK;
+  }
+  if (n > dp.cap) {
+    if (dp.dev) {
+      SA_HIP(hipDeviceSynchronize());   // an in-flight kernel may still read the old plan
+      SA_HIP(hipFree(dp.dev));
+      dp.dev = nullptr;
+    }
+    size_t cap = std::max<size_t>(align_up(n * 2, 4096), 65536);
+    SA_HIP(hipMalloc(&dp.dev, cap));
+    dp.cap = cap;
+  }
+  sa_ctx::Stage& st = ctx->ring[ctx->ring_next];
+  ctx->ring_next = (ctx->ring_next + 1) % kRing;
+  if (st.pending) {
+    SA_HIP(hipEventSynchronize(st.ev));
+    st.pending = false;
+  }
+  if (n > st.cap) {
+    if (st.host) SA_HIP(hipHostFree(st.host));
+    st.host = nullptr;
+    size_t cap = std::max<size_t>(align_up(n * 2, 4096), 65536);
+    SA_HIP(hipHostMalloc(&st.host, cap, hipHostMallocDefault));
+    st.cap = cap;
+  }
+  if (n) {
+    memcpy(st.host, img.bytes.data(), n);
+    SA_HIP(hipMemcpyAsync(dp.dev, st.host, n, hipMemcpyHostToDevice, stream));
+    SA_HIP(hipEventRecord(st.ev, stream));
+    st.pending = true;
+  }
+  dp.shadow = img.bytes;
+  dp.stream = (void*)stream;
+  dp.valid = true;
+  *dev = dp.dev;
+  return SA_OK;
+}
+
+sa_status check_layout(const sa_layout* L) {
+  if (!L) return fail(SA_ERR_NULL, "layout is NULL");
+  if (L->num_q_heads <= 0 || L->num_kv_heads <= 0 || L->num_layers <= 0 || L->num_slots <= 0)
+    return fail(SA_ERR_SHAPE, "layout: heads, layers and slots must be positive");
+  if (L->num_q_heads % L->num_kv_heads != 0)
+    return fail(SA_ERR_SHAPE, "layout: num_q_heads %d is not a multiple of num_kv_heads %d",
+                L->num_q_heads, L->num_kv_heads);
+  if (L->head_dim != 128) return fail(SA_ERR_UNSUPPORTED, "head_dim %d (only 128)", L->head_dim);
+  if (L->page_size != 16 && L->page_size != 32)
+    return fail(SA_ERR_UNSUPPORTED, "page_size %d (only 16 or 32)", L->page_size);
+  const int64_t slot_elems = (int64_t)L->num_kv_heads * L->page_size * 128;
+  if (L->num_slots > INT32_MAX || L->num_slots > (INT64_MAX / 4) / slot_elems / L->num_layers)
+    return fail(SA_ERR_SHAPE, "layout: pool too large");
+  return SA_OK;
+}
+
+int64_t slot_elems(const sa_layout* L) { return (int64_t)L->num_kv_heads * L->page_size * 128; }
+int64_t layer_elems(const sa_layout* L) { return L->num_slots * slot_elems(L); }
+
+sa_status check_ctx(sa_ctx* ctx) {
+  if (!ctx) return fail(SA_ERR_NULL, "context is NULL");
+  SA_HIP(hipSetDevice(ctx->device));
+  return SA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sa_status_string(sa_status s) {
+  switch (s) {
+    case SA_OK: return "ok";
+    case SA_ERR_NULL: return "null pointer";
+    case SA_ERR_SHAPE: return "inconsistent shape or length";
+    case SA_ERR_UNSUPPORTED: return "unsupported configuration";
+    case SA_ERR_ALIGN: return "pointer not 16-byte aligned";
+    case SA_ERR_RANGE: return "value out of range";
+    case SA_ERR_NO_PAGES: return "not enough pages";
+    case SA_ERR_HIP: return "HIP runtime error";
+    case SA_ERR_DEVICE: return "no usable gfx950 device";
+  }
+  return "unknown status";
+}
+
+const char* sa_last_error(void) { return g_err.c_str(); }
+
+sa_status sa_create(int device, sa_ctx** out) {
+  if (!out) return fail(SA_ERR_NULL, "out is NULL");
+  *out = nullptr;
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || device < 0 || device >= n)
+    return fail(SA_ERR_DEVICE, "HIP device %d not present (%d visible)", device, n);
+  hipDeviceProp_t prop;
+  SA_HIP(hipGetDeviceProperties(&prop, device));
+  if (strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+    return fail(SA_ERR_DEVICE, "device %d is %s, not gfx950", device, prop.gcnArchName);
+  SA_HIP(hipSetDevice(device));
+  sa_ctx* c = new sa_ctx();
+  c->device = device;
+  c->num_cu = prop.multiProcessorCount;
+  hipError_t e = hipMalloc(&c->d_err, sizeof(int32_t));
+  if (e == hipSuccess) e = hipMemset(c->d_err, 0, sizeof(int32_t));
+  for (int i = 0; e == hipSuccess && i < kRing; ++i)
+    e = hipEventCreateWithFlags(&c->ring[i].ev, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    sa_destroy(c);
+    return fail(SA_ERR_HIP, "context setup failed: %s", hipGetErrorString(e));
+  }
+  *out = c;
+  return SA_OK;
+}
+
+void sa_destroy(sa_ctx* ctx) {
+  if (!ctx) return;
+  (void)hipSetDevice(ctx->device);
+  (void)hipDeviceSynchronize();
+  for (auto& p : ctx->plans)
+    if (p.dev) (void)hipFree(p.dev);
+  for (auto& s : ctx->ring) {
+    if (s.host) (void)hipHostFree(s.host);
+    if (s.ev) (void)hipEventDestroy(s.ev);
+  }
+  if (ctx->part) (void)hipFree(ctx->part);
+  if (ctx->d_err) (void)hipFree(ctx->d_err);
+  delete ctx;
+}
+
+sa_status sa_sync_check(sa_ctx* ctx, void* stream) {
+  sa_status s = check_ctx(ctx);
+  if (s != SA_OK) return s;
+  SA_HIP(hipStreamSynchronize((hipStream_t)stream));
+  int32_t flag = 0;
+  SA_HIP(hipMemcpy(&flag, ctx->d_err, sizeof flag, hipMemcpyDeviceToHost));
+  if (flag) {
+    SA_HIP(hipMemset(ctx->d_err, 0, sizeof(int32_t)));
+    return fail(SA_ERR_RANGE, "a kernel met an out-of-range page id or slot (flags 0x%x)", flag);
+  }
+  return SA_OK;
+}
+
+// ------------------------------------------------------------------- append
+
+sa_status sa_kv_append(sa_ctx* ctx, const sa_layout* layout, int32_t layer, void* k_pool,
+                       void* v_pool, const void* k_new, const void* v_new, int32_t batch,
+                       const int32_t* h_start, const int32_t* h_new_len, sa_pages pages,
+                       void* stream) {
+  sa_status s = check_layout(layout);
+  if (s != SA_OK) return s;
+  if (layer < 0 || layer >= layout->num_layers)
+    return fail(SA_ERR_SHAPE, "layer %d outside [0, %d)", layer, layout->num_layers);
+  if (batch < 1) return fail(SA_ERR_SHAPE, "batch %d < 1", batch);
+  if (!h_start || !h_new_len) return fail(SA_ERR_NULL, "h_start / h_new_len is NULL");
+  std::vector<int32_t> tok_begin(batch + 1);
+  int64_t total = 0;
+  for (int b = 0; b < batch; ++b) {
+    if (h_start[b] < 0 || h_new_len[b] < 0 || (int64_t)h_start[b] + h_new_len[b] > INT32_MAX)
+      return fail(SA_ERR_SHAPE, "sequence %d: start %d, new_len %d", b, h_start[b], h_new_len[b]);
+    tok_begin[b] = (int32_t)total;
+    total += h_new_len[b];
+    if (total > INT32_MAX / 2) return fail(SA_ERR_SHAPE, "too many new tokens");
+  }
+  tok_begin[batch] = (int32_t)total;
+  if (!k_pool || !v_pool || !pages.indptr || !pages.indices)
+    return fail(SA_ERR_NULL, "pool or page table pointer is NULL");
+  if (total > 0 && (!k_new || !v_new)) return fail(SA_ERR_NULL, "k_new / v_new is NULL");
+  if (!aligned16(k_pool) || !aligned16(v_pool) || !aligned16(k_new) || !aligned16(v_new))
+    return fail(SA_ERR_ALIGN, "pool or new-row pointer not 16-byte aligned");
+  s = check_ctx(ctx);
+  if (s != SA_OK) return s;
+  if (total == 0) return SA_OK;
+
+  PlanImage img;
+  const size_t o_tok = img.add(tok_begin.data(), tok_begin.size());
+  const size_t o_start = img.add(h_start, (size_t)batch);
+  uint8_t* dev = nullptr;
+  s = upload_plan(ctx, kPlanAppend, img, (hipStream_t)stream, &dev);
+  if (s != SA_OK) return s;
+
+  sa::AppendArgs a{};
+  const int64_t lo = (int64_t)layer * layer_elems(layout);
+  a.k_pool = (uint16_t*)k_pool + lo;
+  a.v_pool = (uint16_t*)v_pool + lo;
+  a.k_new = (const uint16_t*)k_new;
+  a.v_new = (const uint16_t*)v_new;
+  a.tok_begin = (const int32_t*)(dev + o_tok);
+  a.start = (const int32_t*)(dev + o_start);
+  a.indptr = pages.indptr;
+  a.indices = pages.indices;
+  a.err = ctx->d_err;
+  a.num_slots = layout->num_slots;
+  a.total_chunks = total * layout->num_kv_heads * 16;
+  a.B = batch;
+  a.Hkv = layout->num_kv_heads;
+  a.P = layout->page_size;
+  const int64_t per_block = 256 * sa::kAppendChunksPerThread;
+  const int64_t blocks = (a.total_chunks + per_block - 1) / per_block;
+  hipLaunchKernelGGL(sa::append_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, a);
+  SA_HIP(hipGetLastError());
+  return SA_OK;
+}
+
+// ----------------------------------------------------------------- assemble
+
+sa_status sa_kv_assemble(sa_ctx* ctx, const sa_layout* layout, const void* k_src,
+                         const void* v_src, void* k_dst, void* v_dst, int32_t batch,
+                         const int32_t* h_src_len, const int32_t* h_keep_indptr,
+                         const int32_t* h_keep_spans, const int32_t* h_reserve, sa_pages src,
+                         const int32_t* d_fresh, int32_t num_fresh, int32_t* d_dst_indptr,
+                         int32_t* d_dst_indices, int32_t dst_capacity, int32_t* h_dst_len,
+                         void* stream) {
+  sa_status s = check_layout(layout);
+  if (s != SA_OK) return s;
+  if (batch < 1) return fail(SA_ERR_SHAPE, "batch %d < 1", batch);
+  if (!h_src_len || !h_keep_indptr || !h_reserve || !h_dst_len)
+    return fail(SA_ERR_NULL, "a host length array is NULL");
+  if (h_keep_indptr[0] != 0) return fail(SA_ERR_SHAPE, "keep_indptr[0] must be 0");
+  if (h_keep_indptr[batch] > 0 && !h_keep_spans) return fail(SA_ERR_NULL, "h_keep_spans is NULL");
+  if (num_fresh < 0 || dst_capacity < 0) return fail(SA_ERR_SHAPE, "negative capacity");
+  const int P = layout->page_size;
+  std::vector<sa::AsmSpan> spans;
+  std::vector<int32_t> dst_indptr(batch + 1, 0), dst_len(batch, 0);
+  int64_t units = 0, n_dst = 0;
+  for (int b = 0; b < batch; ++b) {
+    if (h_src_len[b] < 0 || h_reserve[b] < 0)
+      return fail(SA_ERR_SHAPE, "sequence %d: src_len %d, reserve %d", b, h_src_len[b], h_reserve[b]);
+    if (h_keep_indptr[b + 1] < h_keep_indptr[b])
+      return fail(SA_ERR_SHAPE, "keep_indptr decreases at %d", b);
+    const int n_src_pages = (h_src_len[b] + P - 1) / P;
+    int prev_end = 0, kept_pages = 0;
+    int64_t kept = 0;
+    for (int k = h_keep_indptr[b]; k < h_keep_indptr[b + 1]; ++k) {
+      const int beg = h_keep_spans[2 * k], end = h_keep_spans[2 * k + 1];
+      if (beg < prev_end || beg >= end || end > n_src_pages)
+        return fail(SA_ERR_RANGE, "sequence %d: keep span [%d, %d) invalid (previous end %d, %d pages)",
+                    b, beg, end, prev_end, n_src_pages);
+      spans.push_back({b, beg, kept_pages, (int32_t)units});
+      for (int p = beg; p < end; ++p) kept += std::min(P, h_src_len[b] - p * P);
+      kept_pages += end - beg;
+      units += end - beg;
+      prev_end = end;
+    }
+    const int64_t pages_b = std::max<int64_t>(kept_pages, (kept + h_reserve[b] + P - 1) / P);
+    dst_len[b] = (int32_t)kept;
+    n_dst += pages_b;
+    if (n_dst > INT32_MAX) return fail(SA_ERR_SHAPE, "destination table too large");
+    dst_indptr[b + 1] = (int32_t)n_dst;
+  }
+  if (n_dst > num_fresh)
+    return fail(SA_ERR_NO_PAGES, "need %lld fresh slots, %d given", (long long)n_dst, num_fresh);
+  if (n_dst > dst_capacity)
+    return fail(SA_ERR_NO_PAGES, "destination table needs %lld entries, capacity %d",
+                (long long)n_dst, dst_capacity);
+  if (!k_src || !v_src || !k_dst || !v_dst || !src.indptr || !src.indices || !d_fresh ||
+      !d_dst_indptr || !d_dst_indices)
+    return fail(SA_ERR_NULL, "a device pointer is NULL");
+  if (!aligned16(k_src) || !aligned16(v_src) || !aligned16(k_dst) || !aligned16(v_dst))
+    return fail(SA_ERR_ALIGN, "pool pointer not 16-byte aligned");
+  s = check_ctx(ctx);
+  if (s != SA_OK) return s;
+  memcpy(h_dst_len, dst_len.data(), sizeof(int32_t) * batch);
+
+  PlanImage img;
+  const size_t o_sp = img.add(spans.data(), spans.size());
+  const size_t o_ip = img.add(dst_indptr.data(), dst_indptr.size());
+  uint8_t* dev = nullptr;
+  s = upload_plan(ctx, kPlanAssemble, img, (hipStream_t)stream, &dev);
+  if (s != SA_OK) return s;
+
+  sa::AsmArgs a{};
+  a.k_src = (const uint16_t*)k_src;
+  a.v_src = (const uint16_t*)v_src;
+  a.k_dst = (uint16_t*)k_dst;
+  a.v_dst = (uint16_t*)v_dst;
+  a.spans = (const sa::AsmSpan*)(dev + o_sp);
+  a.dst_indptr = (const int32_t*)(dev + o_ip);
+  a.src_indptr = src.indptr;
+  a.src_indices = src.indices;
+  a.fresh = d_fresh;
+  a.out_indptr = d_dst_indptr;
+  a.out_indices = d_dst_indices;
+  a.err = ctx->d_err;
+  a.num_slots = layout->num_slots;
+  a.slot_elems = slot_elems(layout);
+  a.layer_elems = layer_elems(layout);
+  a.n_spans = (int32_t)spans.size();
+  a.n_units = (int32_t)units;
+  a.n_dst = (int32_t)n_dst;
+  a.B = batch;
+  const int64_t table_blocks = (std::max<int64_t>(n_dst, batch + 1) + 255) / 256;
+  const int64_t gx = std::max<int64_t>(units, table_blocks);
+  hipLaunchKernelGGL(sa::assemble_kernel, dim3((unsigned)gx, (unsigned)layout->num_layers), dim3(256),
+                     0, (hipStream_t)stream, a);
+  SA_HIP(hipGetLastError());
+  return SA_OK;
+}
+
+// ---------------------------------------------------------------- attention
+
+sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t layer,
+                                  const void* q, const void* k_pool, const void* v_pool,
+                                  int32_t batch, const int32_t* h_q_len, const int32_t* h_kv_len,
+                                  sa_pages pages, float softmax_scale, void* o, float* lse,
+                                  void* stream) {
+  sa_status s = check_layout(layout);
+  if (s != SA_OK) return s;
+  if (layer < 0 || layer >= layout->num_layers)
+    return fail(SA_ERR_SHAPE, "layer %d outside [0, %d)", layer, layout->num_layers);
+  if (batch < 1) return fail(SA_ERR_SHAPE, "batch %d < 1", batch);
+  if (!h_q_len || !h_kv_len) return fail(SA_ERR_NULL, "h_q_len / h_kv_len is NULL");
+  if (!std::isfinite(softmax_scale)) return fail(SA_ERR_SHAPE, "softmax_scale is not finite");
+  const int Hq = layout->num_q_heads, Hkv = layout->num_kv_heads, G = Hq / Hkv;
+  std::vector<sa::SeqDesc> seqs(batch);
+  int64_t total_q = 0;
+  for (int b = 0; b < batch; ++b) {
+    if (h_q_len[b] < 0 || h_q_len[b] > h_kv_len[b])
+      return fail(SA_ERR_SHAPE, "sequence %d: need 0 <= q_len (%d) <= kv_len (%d)", b, h_q_len[b],
+                  h_kv_len[b]);
+    if ((int64_t)h_q_len[b] * G > INT32_MAX - sa::kRows)
+      return fail(SA_ERR_SHAPE, "sequence %d: q_len * G too large", b);
+    seqs[b] = {(int32_t)total_q, h_q_len[b], h_kv_len[b], 0};
+    total_q += h_q_len[b];
+    if (total_q > INT32_MAX) return fail(SA_ERR_SHAPE, "too many query tokens");
+  }
+  if (total_q > 0 && (!q || !o)) return fail(SA_ERR_NULL, "q / o is NULL");
+  if (!k_pool || !v_pool || !pages.indptr || !pages.indices)
+    return fail(SA_ERR_NULL, "pool or page table pointer is NULL");
+  if (!aligned16(q) || !aligned16(o) || !aligned16(k_pool) || !aligned16(v_pool) ||
+      (reinterpret_cast<uintptr_t>(lse) & 3u))
+    return fail(SA_ERR_ALIGN, "q, o, pools must be 16-byte aligned (lse 4-byte)");
+  s = check_ctx(ctx);
+  if (s != SA_OK) return s;
+  if (total_q == 0) return SA_OK;
+
+  // ---- work items: (sequence, kv head, 128-row tile), longest first
+  struct Work {
+    sa::AttnItem it;
+    int64_t tiles;
+    bool decode;
+    int xcd;
+  };
+  std::vector<Work> work;
+  int64_t total_tiles = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int ql = h_q_len[b];
+    if (ql == 0) continue;
+    const int rows = ql * G, pre = h_kv_len[b] - ql;
+    for (int g = 0; g < Hkv; ++g)
+      for (int r0 = 0; r0 < rows; r0 += sa::kRows) {
+        const int last = std::min(r0 + sa::kRows - 1, rows - 1);
+        const int kv_end = pre + last / G + 1;
+        const int64_t tiles = (kv_end + sa::kKT - 1) / sa::kKT;
+        work.push_back({{b, g, r0, 0, kv_end, -1}, tiles, rows <= 32, (b * Hkv + g) % kNumXcd});
+        total_tiles += tiles;
+      }
+  }
+  // split long items when there are too few to fill the chip
+  std::vector<sa::MergeGroup> groups;
+  int32_t n_parts = 0;
+  if ((int64_t)work.size() < ctx->num_cu) {
+    const int64_t chunk = std::max<int64_t>(16, (total_tiles + 2 * ctx->num_cu - 1) / (2 * ctx->num_cu));
+    std::vector<Work> split;
+    for (const Work& w : work) {
+      if (w.tiles <= chunk) {
+        split.push_back(w);
+        continue;
+      }
+      const int64_t n = (w.tiles + chunk - 1) / chunk;
+      groups.push_back({w.it.seq, w.it.kvh, w.it.row0, (int32_t)n, n_parts, 0});
+      for (int64_t k = 0; k < n; ++k) {
+        Work p = w;
+        p.it.kv_begin = (int32_t)(k * chunk * sa::kKT);
+        p.it.kv_end = (int32_t)std::min<int64_t>((k + 1) * chunk * sa::kKT, w.it.kv_end);
+        p.it.part = n_parts++;
+        p.tiles = (p.it.kv_end - p.it.kv_begin + sa::kKT - 1) / sa::kKT;
+        split.push_back(p);
+      }
+    }
+    work.swap(split);
+  }
+  std::stable_sort(work.begin(), work.end(), [](const Work& x, const Work& y) {
+    if (x.decode != y.decode) return x.decode;
+    return x.tiles > y.tiles;
+  });
+  // XCD-aware placement: block i runs on XCD i % 8, so all items of one
+  // (sequence, kv head) go to one XCD and share its L2 -- if that balances.
+  int64_t load[kNumXcd] = {0};
+  for (const Work& w : work) load[w.xcd] += w.tiles;
+  const int64_t mx = *std::max_element(load, load + kNumXcd);
+  const int64_t mn = *std::min_element(load, load + kNumXcd);
+  std::vector<sa::AttnItem> items;
+  if (mx > 0 && (double)(mx - mn) <= 0.1 * (double)mx) {
+    std::vector<std::vector<sa::AttnItem>> queue(kNumXcd);
+    for (const Work& w : work) queue[w.xcd].push_back(w.it);
+    size_t depth = 0;
+    for (auto& qd : queue) depth = std::max(depth, qd.size());
+    items.assign(depth * kNumXcd, sa::AttnItem{0, 0, 0, 0, 0, -1});
+    for (int x = 0; x < kNumXcd; ++x)
+      for (size_t i = 0; i < queue[x].size(); ++i) items[i * kNumXcd + x] = queue[x][i];
+  } else {
+    for (const Work& w : work) items.push_back(w.it);
+  }
+
+  if (n_parts > 0) {
+    const size_t need = (size_t)n_parts * sa::kRows * (sa::kHD + 1) * sizeof(float);
+    if (need > ctx->part_cap) {
+      if (ctx->part) {
+        SA_HIP(hipDeviceSynchronize());
+        SA_HIP(hipFree(ctx->part));
+        ctx->part = nullptr;
+      }
+      SA_HIP(hipMalloc(&ctx->part, need));
+      ctx->part_cap = need;
+    }
+  }
+
+  PlanImage img;
+  const size_t o_seq = img.add(seqs.data(), seqs.size());
+  const size_t o_it = img.add(items.data(), items.size());
+  const size_t o_gr = img.add(groups.data(), groups.size());
+  uint8_t* dev = nullptr;
+  s = upload_plan(ctx, kPlanAttn, img, (hipStream_t)stream, &dev);
+  if (s != SA_OK) return s;
+
+  sa::AttnArgs a{};
+  const int64_t lo = (int64_t)layer * layer_elems(layout);
+  a.q = (const uint16_t*)q;
+  a.k = (const uint16_t*)k_pool + lo;
+  a.v = (const uint16_t*)v_pool + lo;
+  a.o = (uint16_t*)o;
+  a.lse = lse;
+  a.part_o = ctx->part;
+  a.part_lse = ctx->part ? ctx->part + (size_t)n_parts * sa::kRows * sa::kHD : nullptr;
+  a.items = (const sa::AttnItem*)(dev + o_it);
+  a.seqs = (const sa::SeqDesc*)(dev + o_seq);
+  a.indptr = pages.indptr;
+  a.indices = pages.indices;
+  a.err = ctx->d_err;
+  a.num_slots = layout->num_slots;
+  a.n_items = (int32_t)items.size();
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.G = G;
+  a.c = softmax_scale * 1.4426950408889634f;
+  if (layout->page_size == 16)
+    hipLaunchKernelGGL(sa::attn_kernel<16>, dim3((unsigned)items.size()), dim3(sa::kThreads), 0,
+                       (hipStream_t)stream, a);
+  else
+    hipLaunchKernelGGL(sa::attn_kernel<32>, dim3((unsigned)items.size()), dim3(sa::kThreads), 0,
+                       (hipStream_t)stream, a);
+  SA_HIP(hipGetLastError());
+  if (!groups.empty()) {
+    sa::MergeArgs m{};
+    m.part_o = a.part_o;
+    m.part_lse = a.part_lse;
+    m.groups = (const sa::MergeGroup*)(dev + o_gr);
+    m.seqs = a.seqs;
+    m.o = a.o;
+    m.lse = lse;
+    m.Hq = Hq;
+    m.G = G;
+    hipLaunchKernelGGL(sa::merge_kernel, dim3((unsigned)groups.size()), dim3(256), 0,
+                       (hipStream_t)stream, m);
+    SA_HIP(hipGetLastError());
+  }
+  return SA_OK;
+}
+
+}  // extern "C"

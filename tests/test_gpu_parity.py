@@ -1,0 +1,328 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Page operations and page tables must match bit for bit (pools are filled with
+a NaN canary first, so stray writes show); attention must be within max-abs
+2e-2 and mean-abs 2e-3 of the double-precision oracle, on every row for small
+cases and on sampled rows at the full configuration sizes.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_00151_amd as sa
+import workloads
+from oracle import pages as opages
+from workloads.configs import build, source_rows
+
+from harness import (attention, build_cache, build_source_cache, compare, dev_i32, dev_u16,
+                     host_u16, layout_of, new_pool, place_range, run_assemble, sample_rows)
+
+pytestmark = pytest.mark.gpu
+
+MAX_TOL, MEAN_TOL = 2e-2, 2e-3
+LSE_TOL = 2e-3
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    print("creating context", flush=True)
+    c = sa.Context(0)
+    yield c
+    c.close()
+
+
+def small(name):
+    if name == "c1":
+        return workloads.make("c1")
+    if name == "ragged_g4_p16":
+        return build(name, 7, 8, 2, 128, 16, [0, 1, 37, 700, 16, 129], [1, 300, 64, 5, 17, 1],
+                     assemble=True)
+    if name == "g8_p32_outliers":
+        return build(name, 8, 16, 2, 128, 32, [0, 513, 31], [77, 200, 1], outlier_frac=0.01,
+                     assemble=True)
+    if name == "g1_p16":
+        return build(name, 9, 4, 4, 128, 16, [33, 0], [40, 130], assemble=True)
+    if name == "g2_p32":
+        return build(name, 10, 8, 4, 128, 32, [100], [100])
+    if name == "g16_p16":
+        return build(name, 11, 32, 2, 128, 16, [64, 3], [50, 9])
+    if name == "g3_p16":
+        return build(name, 12, 6, 2, 128, 16, [45, 0, 300], [43, 70, 2], assemble=True)
+    raise KeyError(name)
+
+
+SMALL = ["c1", "ragged_g4_p16", "g8_p32_outliers", "g1_p16", "g2_p32", "g16_p16", "g3_p16"]
+WITH_ASM = ["ragged_g4_p16", "g8_p32_outliers", "g1_p16", "g3_p16"]
+
+
+def oracle_all(w):
+    return oracle.attention_all(w.q, w.k, w.v, w.q_indptr, w.kv_indptr, w.num_q_heads,
+                                w.num_kv_heads, w.scale)
+
+
+# ------------------------------------------------------------------ append
+
+@pytest.mark.parametrize("name", SMALL)
+def test_append_bitexact(ctx, name):
+    print(f"append {name}", flush=True)
+    w = small(name)
+    L = layout_of(w, num_layers=2)
+    kp, vp = new_pool(w, 2), new_pool(w, 2)
+    layer = 1
+    # prefix placed by the harness, segment appended by the kernel
+    for pool, full in ((kp, w.k), (vp, w.v)):
+        place_range(pool, layer, w, lambda b, full=full: full[w.prefix_rows(b)], w.pages_indptr,
+                    w.pages, w.pre)
+    before_k, before_v = host_u16(kp), host_u16(vp)
+    indptr, indices = dev_i32(w.pages_indptr), dev_i32(w.pages)
+    sa.sa_kv_append(ctx, L, layer, kp, vp, dev_u16(w.k_seg()), dev_u16(w.v_seg()), w.pre, w.qlen,
+                    indptr, indices)
+    sa.sa_sync_check(ctx)
+    sl, ro = opages.append_destinations(w.pre, w.qlen, w.pages_indptr, w.pages, w.page_size)
+    for before, new, got in ((before_k, w.k_seg(), kp), (before_v, w.v_seg(), vp)):
+        want = before.copy()
+        opages.apply_append(want[layer], new, sl, ro)
+        assert np.array_equal(host_u16(got), want)
+
+
+# ---------------------------------------------------------------- assemble
+
+@pytest.mark.parametrize("name", WITH_ASM)
+def test_assemble_bitexact(ctx, name):
+    print(f"assemble {name}", flush=True)
+    w = small(name)
+    a = w.asm
+    L = layout_of(w, num_layers=2)
+    kp, vp, sip, sid, fresh = build_source_cache(w, num_layers=2)
+    before_k, before_v = host_u16(kp), host_u16(vp)
+    dip, did, dst_len = run_assemble(ctx, w, L, kp, vp, sip, sid, fresh)
+    sa.sa_sync_check(ctx)
+    r = opages.assemble(a.src_len, a.src_indptr, a.src_indices, a.keep_indptr, a.keep_spans,
+                        a.reserve, a.fresh, w.page_size)
+    assert np.array_equal(dst_len, r["dst_len"])
+    assert np.array_equal(dip.cpu().numpy(), r["dst_indptr"])
+    n = int(r["dst_indptr"][-1])
+    assert np.array_equal(did.cpu().numpy()[:n], r["dst_indices"])
+    assert (did.cpu().numpy()[n:] == -1).all()
+    for before, got in ((before_k, kp), (before_v, vp)):
+        want = before.copy()
+        want[:, r["copy_dst"]] = before[:, r["copy_src"]]
+        assert np.array_equal(host_u16(got), want)
+    # the kept prefix reads back as the workload's prefix rows
+    g = host_u16(kp)[0]
+    for b in range(w.batch):
+        got = opages.gather_logical(g, r["dst_indptr"][b:], r["dst_indices"], [r["dst_len"][b]],
+                                    w.page_size, 0)
+        assert np.array_equal(got, w.k[w.prefix_rows(b)])
+
+
+# --------------------------------------------------------------- attention
+
+@pytest.mark.parametrize("name", SMALL)
+def test_attention_all_rows(ctx, name):
+    print(f"attention {name}", flush=True)
+    w = small(name)
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    o, lse = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    sa.sa_sync_check(ctx)
+    ref, ref_lse, _ = oracle_all(w)
+    mx, mean = compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
+    print(f"  max {mx:.3e} mean {mean:.3e}")
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() <= LSE_TOL
+
+
+def test_split_kv_and_merge(ctx):
+    """Few long work items force key-range splits and the LSE merge."""
+    w = build("split", 21, 8, 1, 128, 16, [5000, 3000, 70, 0], [1, 1, 3, 1])
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    o, lse = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    sa.sa_sync_check(ctx)
+    ref, ref_lse, _ = oracle_all(w)
+    compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() <= LSE_TOL
+
+
+def test_page_permutation_invariance(ctx):
+    """Where the pages sit in the pool does not change a single output bit."""
+    w = workloads.make("c1")
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    o1, _ = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    w2 = workloads.make("c1")
+    w2.pages = np.arange(len(w.pages), dtype=np.int32)[::-1].copy()
+    kp2, vp2, ip2, ix2 = build_cache(w2)
+    o2, _ = attention(ctx, w2, L, dev_u16(w.q), kp2, vp2, ip2, ix2)
+    assert torch.equal(o1, o2)
+
+
+def test_causality(ctx):
+    """Changing the K/V of segment tokens after t leaves rows <= t bit-identical."""
+    w = build("causal", 31, 8, 2, 128, 16, [40], [100])
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    q = dev_u16(w.q)
+    base, _ = attention(ctx, w, L, q, kp, vp, ip, ix)
+    for t in (0, 37, 63, 98):
+        w2 = build("causal", 31, 8, 2, 128, 16, [40], [100])
+        cut = int(w.pre[0]) + t + 1
+        w2.k[cut:] = workloads.rng.normal_bf16(500 + t, 1, w2.k[cut:].shape)
+        w2.v[cut:] = workloads.rng.normal_bf16(600 + t, 2, w2.v[cut:].shape)
+        kp2, vp2, _, _ = build_cache(w2)
+        o2, _ = attention(ctx, w2, L, q, kp2, vp2, ip, ix)
+        assert torch.equal(o2[: t + 1], base[: t + 1]), t
+        assert not torch.equal(o2[t + 1:], base[t + 1:]), t
+
+
+def test_chunked_prefill_matches_one_shot(ctx):
+    """Segment decomposability on the device: append + attend chunk by chunk
+    over the growing cache gives the one-shot rows (within tolerance of the
+    oracle, and of each other)."""
+    w = build("chunks", 41, 8, 2, 128, 16, [200], [300])
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w, with_segment=False)
+    q = dev_u16(w.q)
+    seg_k, seg_v = w.k_seg(), w.v_seg()
+    outs = []
+    for a, b in ((0, 77), (77, 200), (200, 300)):
+        sa.sa_kv_append(ctx, L, 0, kp, vp, dev_u16(seg_k[a:b]), dev_u16(seg_v[a:b]),
+                        [200 + a], [b - a], ip, ix)
+        o = torch.empty((b - a, 8, 128), dtype=torch.int16, device="cuda")
+        sa.sa_segment_prefill_attn(ctx, L, 0, q[a:b].contiguous(), kp, vp, [b - a], [200 + b], ip,
+                                   ix, w.scale, o)
+        outs.append(o)
+    chunked = torch.cat(outs)
+    one, _ = attention(ctx, w, L, q, kp, vp, ip, ix)
+    sa.sa_sync_check(ctx)
+    ref, _, _ = oracle_all(w)
+    compare(host_u16(chunked), ref, MAX_TOL, MEAN_TOL)
+    compare(host_u16(one), ref, MAX_TOL, MEAN_TOL)
+
+
+def test_out_of_range_slot_is_reported(ctx):
+    """A slot id beyond the pool is skipped by the kernels and reported."""
+    w = workloads.make("c1")
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    bad = w.pages.copy()
+    bad[3] = w.num_slots + 5
+    o, _ = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, dev_i32(bad))
+    with pytest.raises(sa.SaError) as e:
+        sa.sa_sync_check(ctx)
+    assert e.value.name == "SA_ERR_RANGE"
+    sa.sa_sync_check(ctx)           # flag cleared
+
+
+# ------------------------------------------------------ whole step, full size
+
+def run_step(ctx, w, L, state):
+    """assemble (commit splice) -> append (segment) -> attention, as timed by the bench."""
+    kp, vp, sip, sid, fresh, dip, did, q, ks, vs, o, lse = state
+    a = w.asm
+    dst_len = sa.sa_kv_assemble(ctx, L, kp, vp, kp, vp, a.src_len, a.keep_indptr, a.keep_spans,
+                                a.reserve, sip, sid, fresh, dip, did)
+    sa.sa_kv_append(ctx, L, 0, kp, vp, ks, vs, dst_len, w.qlen, dip, did)
+    sa.sa_segment_prefill_attn(ctx, L, 0, q, kp, vp, w.qlen, dst_len + w.qlen, dip, did, w.scale,
+                               o, lse)
+    return dst_len
+
+
+def check_step(ctx, w, per_seq_rows):
+    L = layout_of(w)
+    kp, vp, sip, sid, fresh = build_source_cache(w)
+    n_dst = len(w.asm.fresh)
+    dip = torch.zeros(w.batch + 1, dtype=torch.int32, device="cuda")
+    did = torch.full((n_dst,), -1, dtype=torch.int32, device="cuda")
+    T = int(w.qlen.sum())
+    o = torch.empty((T, w.num_q_heads, 128), dtype=torch.int16, device="cuda")
+    lse = torch.empty((T, w.num_q_heads), dtype=torch.float32, device="cuda")
+    state = (kp, vp, sip, sid, fresh, dip, did, dev_u16(w.q), dev_u16(w.k_seg()),
+             dev_u16(w.v_seg()), o, lse)
+    dst_len = run_step(ctx, w, L, state)
+    sa.sa_sync_check(ctx)
+    assert np.array_equal(dst_len, w.pre)
+    # the assembled cache reads back as prefix ++ segment, bit for bit (sampled sequences)
+    r = opages.assemble(w.asm.src_len, w.asm.src_indptr, w.asm.src_indices, w.asm.keep_indptr,
+                        w.asm.keep_spans, w.asm.reserve, w.asm.fresh, w.page_size)
+    assert np.array_equal(dip.cpu().numpy(), r["dst_indptr"])
+    assert np.array_equal(did.cpu().numpy()[: r["dst_indptr"][-1]], r["dst_indices"])
+    ip_h, ix_h = r["dst_indptr"], r["dst_indices"]
+    for b in sorted({0, w.batch - 1}):
+        pages_b = ix_h[ip_h[b]: ip_h[b + 1]]
+        kv_b = int(w.kv[b])
+        for pool, full in ((kp, w.k), (vp, w.v)):
+            got = pool[0][torch.from_numpy(pages_b.astype(np.int64)).cuda()]
+            got = host_u16(got)                               # [pages][Hkv][P][D]
+            got = got.transpose(0, 2, 1, 3).reshape(-1, w.num_kv_heads, 128)[:kv_b]
+            assert np.array_equal(got, full[int(w.kv_indptr[b]): int(w.kv_indptr[b]) + kv_b]), b
+    # attention on sampled rows
+    toks, heads = sample_rows(w, per_seq_rows)
+    ref, ref_lse, _ = oracle.attention_rows(w.q, w.k, w.v, w.q_indptr, w.kv_indptr,
+                                            w.num_q_heads, w.num_kv_heads, w.scale, toks, heads)
+    got = host_u16(o)[toks, heads]
+    mx, mean = compare(got, ref, MAX_TOL, MEAN_TOL)
+    print(f"  {w.name}: {len(toks)} rows, max {mx:.3e} mean {mean:.3e}", flush=True)
+    assert np.abs(lse.cpu().numpy()[toks, heads] - ref_lse).max() <= LSE_TOL
+    assert torch.isfinite(o.view(torch.bfloat16).float()).all()
+
+
+@pytest.mark.parametrize("name", WITH_ASM)
+def test_step_small(ctx, name):
+    check_step(ctx, small(name), per_seq_rows=64)
+
+
+@pytest.mark.timeout(600)
+def test_step_c2_full(ctx):
+    print("c2 full step", flush=True)
+    check_step(ctx, workloads.make("c2"), per_seq_rows=512)
+
+
+@pytest.mark.timeout(900)
+def test_step_c3_full(ctx):
+    print("c3 full step", flush=True)
+    check_step(ctx, workloads.make("c3"), per_seq_rows=48)
+
+
+def check_direct(ctx, w, per_seq_rows, extra_rows=None):
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w, with_segment=False)
+    sa.sa_kv_append(ctx, L, 0, kp, vp, dev_u16(w.k_seg()), dev_u16(w.v_seg()), w.pre, w.qlen,
+                    ip, ix)
+    o, lse = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    sa.sa_sync_check(ctx)
+    toks, heads = sample_rows(w, per_seq_rows)
+    if extra_rows is not None:
+        toks = np.concatenate([toks, extra_rows[0]])
+        heads = np.concatenate([heads, extra_rows[1]])
+    ref, ref_lse, _ = oracle.attention_rows(w.q, w.k, w.v, w.q_indptr, w.kv_indptr,
+                                            w.num_q_heads, w.num_kv_heads, w.scale, toks, heads)
+    mx, mean = compare(host_u16(o)[toks, heads], ref, MAX_TOL, MEAN_TOL)
+    print(f"  {w.name}: {len(toks)} rows, max {mx:.3e} mean {mean:.3e}", flush=True)
+    assert np.abs(lse.cpu().numpy()[toks, heads] - ref_lse).max() <= LSE_TOL
+    assert torch.isfinite(o.view(torch.bfloat16).float()).all()
+
+
+@pytest.mark.timeout(600)
+def test_c1_full(ctx):
+    check_direct(ctx, workloads.make("c1"), per_seq_rows=256)
+
+
+@pytest.mark.timeout(900)
+def test_c4_full_outliers(ctx):
+    print("c4 full", flush=True)
+    w = workloads.make("c4")
+    # rows whose own position is right after an outlier key: those keys dominate their softmax
+    out_tok = (w.outlier_rows // w.num_kv_heads) - int(w.pre[0])
+    out_kvh = w.outlier_rows % w.num_kv_heads
+    sel = (out_tok >= 0) & (out_tok < int(w.qlen[0]))
+    G = w.num_q_heads // w.num_kv_heads
+    extra = (out_tok[sel][:64].astype(np.int64), (out_kvh[sel][:64] * G).astype(np.int32))
+    check_direct(ctx, w, per_seq_rows=160, extra_rows=extra)
+
+
+@pytest.mark.timeout(600)
+def test_c5_full_mixed(ctx):
+    print("c5 full", flush=True)
+    check_direct(ctx, workloads.make("c5"), per_seq_rows=24)

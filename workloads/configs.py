@@ -179,10 +179,14 @@ def build(name: str, seed: int, Hq: int, Hkv: int, D: int, P: int,
         spans, keep_indptr = [], [0]
         for b in range(B):
             a, nd, ns = int(asm_drop_at[b]), int(asm_n_drop[b]), n_src_pages[b]
-            if a > 0:
-                spans.append((0, a))
-            if a + nd < ns:
-                spans.append((a + nd, ns))
+            if nd == 0:                       # too short to drop a whole page
+                if ns > 0:
+                    spans.append((0, ns))
+            else:
+                if a > 0:
+                    spans.append((0, a))
+                if a + nd < ns:
+                    spans.append((a + nd, ns))
             keep_indptr.append(len(spans))
         n_drop_tok = int((asm_n_drop * P).sum())
         asm = AssembleInputs(
