@@ -182,7 +182,8 @@ sa_status sa_kv_assemble(sa_ctx *ctx, const sa_layout *layout,
  * accumulation, fp32 online softmax, probabilities rounded to bf16 before the
  * PV product.
  *
- * Errors: SA_ERR_SHAPE (0 <= q_len <= kv_len violated, bad batch or layer),
+ * Errors: SA_ERR_SHAPE (0 <= q_len <= kv_len violated, bad batch or layer,
+ * softmax_scale not finite and positive),
  * SA_ERR_UNSUPPORTED, SA_ERR_NULL, SA_ERR_ALIGN, SA_ERR_HIP.
  */
 sa_status sa_segment_prefill_attn(sa_ctx *ctx, const sa_layout *layout, int32_t layer,

@@ -14,6 +14,8 @@ HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     # packed fp32 VALU forms stay out of every kernel
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # keep small per-thread arrays in registers, not in LDS
+    "-mllvm", "-disable-promote-alloca-to-lds",
     "-Wall", "-Wno-unused-command-line-argument",
 ]
 

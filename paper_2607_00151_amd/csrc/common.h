@@ -16,6 +16,21 @@ __device__ __forceinline__ u32x4 ld_u32x4(const uint16_t* p) { return *(const u3
 __device__ __forceinline__ bf16x8 ld_bf16x8(const uint16_t* p) { return *(const bf16x8*)p; }
 __device__ __forceinline__ void st_u32x4(uint16_t* p, u32x4 v) { *(u32x4*)p = v; }
 
+// Load through the constant address space: for a wave-uniform address this is
+// a scalar (s_load) read.  Only for data no kernel writes while it runs.
+template <typename T>
+__device__ __forceinline__ T ld_uniform(const T* p) {
+  static_assert(sizeof(T) % 4 == 0, "word-sized types only");
+  typedef const __attribute__((address_space(4))) uint32_t cu32;
+  cu32* q = (cu32*)p;
+  uint32_t w[sizeof(T) / 4];
+#pragma unroll
+  for (unsigned i = 0; i < sizeof(T) / 4; ++i) w[i] = q[i];
+  T out;
+  __builtin_memcpy(&out, w, sizeof(T));
+  return out;
+}
+
 // v_exp_f32: 2^x (exp2(-inf) = 0).
 __device__ __forceinline__ float exp2f_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 

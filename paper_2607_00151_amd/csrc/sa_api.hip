@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -152,6 +153,38 @@ sa_status check_ctx(sa_ctx* ctx) {
   if (!ctx) return fail(SA_ERR_NULL, "context is NULL");
   SA_HIP(hipSetDevice(ctx->device));
   return SA_OK;
+}
+
+// Attention kernel variants: 32 * qt query rows per wave, `waves` waves per
+// work item.  SA_ATTN_VARIANT overrides the default (tuning only).
+struct AttnVariant {
+  int qt, waves;
+};
+constexpr AttnVariant kVariants[] = {{1, 4}, {2, 2}, {2, 4}};
+constexpr int kDefaultVariant = 0;
+
+AttnVariant attn_variant() {
+  static int v = [] {
+    const char* e = getenv("SA_ATTN_VARIANT");
+    int x = e ? atoi(e) : kDefaultVariant;
+    return (x >= 0 && x < (int)(sizeof(kVariants) / sizeof(kVariants[0]))) ? x : kDefaultVariant;
+  }();
+  return kVariants[v];
+}
+
+template <int P>
+void launch_attn_p(AttnVariant v, dim3 grid, hipStream_t st, const sa::AttnArgs& a) {
+  if (v.qt == 1 && v.waves == 4)
+    hipLaunchKernelGGL((sa::attn_kernel<P, 1, 4>), grid, dim3(256), 0, st, a);
+  else if (v.qt == 2 && v.waves == 2)
+    hipLaunchKernelGGL((sa::attn_kernel<P, 2, 2>), grid, dim3(128), 0, st, a);
+  else
+    hipLaunchKernelGGL((sa::attn_kernel<P, 2, 4>), grid, dim3(256), 0, st, a);
+}
+
+void launch_attn(int page_size, AttnVariant v, dim3 grid, hipStream_t st, const sa::AttnArgs& a) {
+  if (page_size == 16) launch_attn_p<16>(v, grid, st, a);
+  else launch_attn_p<32>(v, grid, st, a);
 }
 
 }  // namespace
@@ -398,7 +431,8 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
     return fail(SA_ERR_SHAPE, "layer %d outside [0, %d)", layer, layout->num_layers);
   if (batch < 1) return fail(SA_ERR_SHAPE, "batch %d < 1", batch);
   if (!h_q_len || !h_kv_len) return fail(SA_ERR_NULL, "h_q_len / h_kv_len is NULL");
-  if (!std::isfinite(softmax_scale)) return fail(SA_ERR_SHAPE, "softmax_scale is not finite");
+  if (!std::isfinite(softmax_scale) || softmax_scale <= 0.f)
+    return fail(SA_ERR_SHAPE, "softmax_scale must be finite and positive");
   const int Hq = layout->num_q_heads, Hkv = layout->num_kv_heads, G = Hq / Hkv;
   std::vector<sa::SeqDesc> seqs(batch);
   int64_t total_q = 0;
@@ -406,7 +440,7 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
     if (h_q_len[b] < 0 || h_q_len[b] > h_kv_len[b])
       return fail(SA_ERR_SHAPE, "sequence %d: need 0 <= q_len (%d) <= kv_len (%d)", b, h_q_len[b],
                   h_kv_len[b]);
-    if ((int64_t)h_q_len[b] * G > INT32_MAX - sa::kRows)
+    if ((int64_t)h_q_len[b] * G > INT32_MAX - sa::kMaxRows)
       return fail(SA_ERR_SHAPE, "sequence %d: q_len * G too large", b);
     seqs[b] = {(int32_t)total_q, h_q_len[b], h_kv_len[b], 0};
     total_q += h_q_len[b];
@@ -422,7 +456,11 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
   if (s != SA_OK) return s;
   if (total_q == 0) return SA_OK;
 
-  // ---- work items: (sequence, kv head, 128-row tile), longest first
+  // ---- kernel variant: query rows per wave (32 * qt) and waves per work item
+  const AttnVariant var = attn_variant();
+  const int rows_item = 32 * var.qt * var.waves;
+
+  // ---- work items: (sequence, kv head, row tile), longest first
   struct Work {
     sa::AttnItem it;
     int64_t tiles;
@@ -436,8 +474,8 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
     if (ql == 0) continue;
     const int rows = ql * G, pre = h_kv_len[b] - ql;
     for (int g = 0; g < Hkv; ++g)
-      for (int r0 = 0; r0 < rows; r0 += sa::kRows) {
-        const int last = std::min(r0 + sa::kRows - 1, rows - 1);
+      for (int r0 = 0; r0 < rows; r0 += rows_item) {
+        const int last = std::min(r0 + rows_item - 1, rows - 1);
         const int kv_end = pre + last / G + 1;
         const int64_t tiles = (kv_end + sa::kKT - 1) / sa::kKT;
         work.push_back({{b, g, r0, 0, kv_end, -1}, tiles, rows <= 32, (b * Hkv + g) % kNumXcd});
@@ -492,7 +530,7 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
   }
 
   if (n_parts > 0) {
-    const size_t need = (size_t)n_parts * sa::kRows * (sa::kHD + 1) * sizeof(float);
+    const size_t need = (size_t)n_parts * rows_item * (sa::kHD + 1) * sizeof(float);
     if (need > ctx->part_cap) {
       if (ctx->part) {
         SA_HIP(hipDeviceSynchronize());
@@ -520,24 +558,19 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
   a.o = (uint16_t*)o;
   a.lse = lse;
   a.part_o = ctx->part;
-  a.part_lse = ctx->part ? ctx->part + (size_t)n_parts * sa::kRows * sa::kHD : nullptr;
+  a.part_lse = ctx->part ? ctx->part + (size_t)n_parts * rows_item * sa::kHD : nullptr;
   a.items = (const sa::AttnItem*)(dev + o_it);
   a.seqs = (const sa::SeqDesc*)(dev + o_seq);
   a.indptr = pages.indptr;
   a.indices = pages.indices;
   a.err = ctx->d_err;
-  a.num_slots = layout->num_slots;
+  a.num_slots = (int32_t)layout->num_slots;
   a.n_items = (int32_t)items.size();
   a.Hq = Hq;
   a.Hkv = Hkv;
   a.G = G;
   a.c = softmax_scale * 1.4426950408889634f;
-  if (layout->page_size == 16)
-    hipLaunchKernelGGL(sa::attn_kernel<16>, dim3((unsigned)items.size()), dim3(sa::kThreads), 0,
-                       (hipStream_t)stream, a);
-  else
-    hipLaunchKernelGGL(sa::attn_kernel<32>, dim3((unsigned)items.size()), dim3(sa::kThreads), 0,
-                       (hipStream_t)stream, a);
+  launch_attn(layout->page_size, var, dim3((unsigned)items.size()), (hipStream_t)stream, a);
   SA_HIP(hipGetLastError());
   if (!groups.empty()) {
     sa::MergeArgs m{};
@@ -549,6 +582,7 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
     m.lse = lse;
     m.Hq = Hq;
     m.G = G;
+    m.rows = rows_item;
     hipLaunchKernelGGL(sa::merge_kernel, dim3((unsigned)groups.size()), dim3(256), 0,
                        (hipStream_t)stream, m);
     SA_HIP(hipGetLastError());
