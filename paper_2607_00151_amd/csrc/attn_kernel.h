@@ -107,14 +107,16 @@ __device__ __forceinline__ float pair_sum(float x) {
 template <int P, int QT, int WAVES>
 __global__ __launch_bounds__(64 * WAVES, (QT == 1 ? 2 : 1)) void attn_kernel(AttnArgs a) {
   static_assert(P == 16 || P == 32, "page size");
-  static_assert(16 % WAVES == 0, "waves must divide the 16 loads of a tile");
+  static_assert(16 % WAVES == 0 && (WAVES & (WAVES - 1)) == 0, "waves: a power of two dividing 16");
   constexpr int kRowsW = 32 * QT;                          // rows per wave
   constexpr int kRows = kRowsW * WAVES;                    // rows per item
   constexpr int kTileBytes = kKT * kHD * 2;                // 16 KB
   constexpr int kPagesPerTile = kKT / P;
   constexpr int kNJ = 16 / WAVES;                          // loads per wave per tile and operand
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[4 * kTileBytes];  // 2 x (K, V)
-  lds_u8* lds = (lds_u8*)smem;
+  // one array per buffer: distinct objects let the compiler see that the DMA
+  // writes into one buffer never alias the operand reads of the other
+  __shared__ __attribute__((aligned(1024))) uint8_t k_lds0[kTileBytes], k_lds1[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t v_lds0[kTileBytes], v_lds1[kTileBytes];
 
   const AttnItem it = ld_uniform(a.items + blockIdx.x);
   if (it.kv_begin >= it.kv_end) return;                     // padding item
@@ -122,7 +124,8 @@ __global__ __launch_bounds__(64 * WAVES, (QT == 1 ? 2 : 1)) void attn_kernel(Att
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // the mask tells the compiler wave < WAVES, so per-load page indices fold to constants
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & (WAVES - 1);
   const int hh = lane >> 5;                                 // lane half
   const int G = a.G;
   const int rows_total = sd.q_len * G;
@@ -190,11 +193,9 @@ __global__ __launch_bounds__(64 * WAVES, (QT == 1 ? 2 : 1)) void attn_kernel(Att
   };
   auto slot_ok = [&](int32_t s) { return s >= 0 && s < a.num_slots; };
 
-  // issue the global -> LDS loads of tile t into buffer buf
-  auto load_tile = [&](int t, const Slots& S, int buf) {
+  // issue the global -> LDS loads of tile t into the buffers kb, vb
+  auto load_tile = [&](int t, const Slots& S, lds_u8* kb, lds_u8* vb) {
     const int ts = t * kKT;
-    lds_u8* kb = lds + buf * 2 * kTileBytes;
-    lds_u8* vb = kb + kTileBytes;
     bool fast = ts + kKT <= it.kv_end;
 #pragma unroll
     for (int j = 0; j < kPagesPerTile; ++j) fast = fast && slot_ok(S.s[j]);
@@ -254,20 +255,23 @@ __global__ __launch_bounds__(64 * WAVES, (QT == 1 ? 2 : 1)) void attn_kernel(Att
 
   const int t0 = it.kv_begin / kKT;
   const int t1 = (it.kv_end + kKT - 1) / kKT;
-  load_tile(t0, fetch(t0), 0);
+  lds_u8* const K0 = (lds_u8*)k_lds0;
+  lds_u8* const K1 = (lds_u8*)k_lds1;
+  lds_u8* const V0 = (lds_u8*)v_lds0;
+  lds_u8* const V1 = (lds_u8*)v_lds1;
+  load_tile(t0, fetch(t0), K0, V0);
   Slots nxt = fetch(t0 + 1 < t1 ? t0 + 1 : t0);
-  for (int t = t0; t < t1; ++t) {
-    const int buf = (t - t0) & 1;
+
+  // one key tile: wait for its loads, start the next tile's, compute
+  auto step = [&](int t, const lds_u8* kb, const lds_u8* vb, lds_u8* kn, lds_u8* vn) {
     __builtin_amdgcn_s_waitcnt(0x0070);                     // vmcnt(0) lgkmcnt(0): my loads landed
-    __syncthreads();                                        // everyone's landed; buf ^ 1 is free
+    __syncthreads();                                        // everyone's landed; kn, vn are free
     if (t + 1 < t1) {
-      load_tile(t + 1, nxt, buf ^ 1);
+      load_tile(t + 1, nxt, kn, vn);
       if (t + 2 < t1) nxt = fetch(t + 2);
     }
     const int ts = t * kKT;
-    if (wave_active && ts < w_kv_end) {
-      const lds_u8* kb = lds + buf * 2 * kTileBytes;
-      const lds_u8* vb = kb + kTileBytes;
+    if (!(wave_active && ts < w_kv_end)) return;
       f32x16 s[2][QT];
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
@@ -343,7 +347,10 @@ __global__ __launch_bounds__(64 * WAVES, (QT == 1 ? 2 : 1)) void attn_kernel(Att
             oacc[dt][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[qt][kb2], oacc[dt][qt], 0, 0, 0);
         }
       }
-    }
+  };
+  for (int t = t0; t < t1; t += 2) {
+    step(t, K0, V0, K1, V1);
+    if (t + 1 < t1) step(t + 1, K1, V1, K0, V0);
   }
 
   if (!wave_active) return;
