@@ -40,8 +40,60 @@ def parse():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--rotate", type=int, default=8, help="disjoint cache copies cycled per step")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-stride", type=int, default=16, help="oracle sample: every n-th token")
+    p.add_argument("--cpu-stride", type=int, default=1, help="oracle sample: every n-th token")
+    p.add_argument("--assemble-layers", type=int, default=32,
+                   help="layers of the separate all-layer assemble measurement (0: skip)")
+    p.add_argument("--copy-bytes", type=int, default=0,
+                   help="instead of the step, time a plain device copy of this many bytes "
+                        "(calibrates the FETCH_SIZE / WRITE_SIZE counters)")
     return p.parse_args()
+
+
+def source_digest() -> str:
+    """Hash of the attention kernel sources; counter figures taken for another
+    version of the kernel are not reported."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("attn_kernel.h", "common.h"):
+        with open(os.path.join(ROOT, "paper_2607_00151_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(kernel: str, algorithmic: float):
+    """HBM bytes per launch from the committed counter summary, if it was taken
+    on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    k = t.get("kernels", {}).get(kernel)
+    if not k or k.get("source_digest") != source_digest():
+        return None
+    fetch = k["fetch_kib_per_launch"] * 1024 * t["copy_calibration"]["fetch_factor"]
+    write = k["write_kib_per_launch"] * 1024 * t["copy_calibration"]["write_factor"]
+    return {"bytes": fetch + write, "fetch_bytes": fetch, "write_bytes": write,
+            "algorithmic_bytes": algorithmic, "ratio_to_algorithmic": (fetch + write) / algorithmic}
+
+
+def copy_mode(nbytes: int, steps: int, warmup: int):
+    import torch
+    n = nbytes // 2
+    src = torch.empty(n, dtype=torch.int16, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(warmup):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    print(json.dumps({"mode": "copy", "bytes_read": 2 * n, "bytes_written": 2 * n,
+                      "ms": ms, "gbs": 4 * n / (ms * 1e-3) / 1e9}), flush=True)
 
 
 def main():
@@ -50,6 +102,9 @@ def main():
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
+    if args.copy_bytes:
+        copy_mode(args.copy_bytes, args.steps, args.warmup)
+        return
 
     import torch
     import paper_2607_00151_amd as sa
@@ -138,6 +193,9 @@ def main():
     app_bytes = 2 * T * Hkv * D * 2 * 2                   # K and V rows, read + write
     flops = w.attn_flops()
     attn_tflops = flops / (attn_ms * 1e-3) / 1e12
+    # compulsory attention bytes: Q, the cache rows it reads, O and LSE
+    attn_bytes = (T * w.num_q_heads * 128 * 2 + int(w.kv.sum()) * Hkv * 128 * 2 * 2
+                  + T * w.num_q_heads * 128 * 2 + T * w.num_q_heads * 4)
 
     rec = {
         "metric": "segment-prefill tokens/s + attn TFLOP/s (% MFMA peak); KV assemble GB/s (% HBM)",
@@ -166,10 +224,42 @@ def main():
                      "frac_of_hbm": asm_bytes / (asm_ms * 1e-3) / 1e9 / PEAK_HBM_GBS},
         "append": {"ms": app_ms, "bytes": app_bytes, "gbs": app_bytes / (app_ms * 1e-3) / 1e9},
         "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": attn_tflops / PEAK_BF16_TFLOPS, "traffic": None},
+                     "unit": "TFLOP/s", "frac": attn_tflops / PEAK_BF16_TFLOPS,
+                     "traffic": stored_traffic("attn_kernel", attn_bytes)},
         "paper_context": "paper reports up to 11.9x transform-point TTFT reduction end to end on "
                          "H100 80GB (SGLang, Qwen3-8B); no kernel-level numbers",
     }
+
+    if args.assemble_layers > 0:
+        # the commit splice of every layer of the model in one launch: the same
+        # page plan applied to pools that hold num_layers layers
+        NL = args.assemble_layers
+        L2 = sa.Layout(num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads, head_dim=128,
+                       page_size=w.page_size, num_layers=NL, num_slots=base_slots)
+        kl = torch.empty((NL, base_slots, Hkv, P, D), dtype=torch.int16, device="cuda")
+        vl = torch.empty_like(kl)
+        kl[:] = kp[0, :base_slots]
+        vl[:] = vp[0, :base_slots]
+        c0 = copies[0]
+        evl = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        for i in range(3):
+            sa.sa_kv_assemble(ctx, L2, kl, vl, kl, vl, a.src_len, a.keep_indptr, a.keep_spans,
+                              a.reserve, c0["sip"], c0["sid"], c0["fresh"], c0["dip"], c0["did"])
+        torch.cuda.synchronize()
+        reps = 10
+        evl[0].record(stream)
+        for i in range(reps):
+            sa.sa_kv_assemble(ctx, L2, kl, vl, kl, vl, a.src_len, a.keep_indptr, a.keep_spans,
+                              a.reserve, c0["sip"], c0["sid"], c0["fresh"], c0["dip"], c0["did"])
+        evl[1].record(stream)
+        torch.cuda.synchronize()
+        sa.sa_sync_check(ctx)
+        ms_l = evl[0].elapsed_time(evl[1]) / reps
+        bytes_l = 2 * kept_pages * page_bytes * NL + 4 * (n_dst + kept_pages + w.batch + 1)
+        rec["assemble_all_layers"] = {
+            "layers": NL, "ms": ms_l, "bytes": bytes_l, "gbs": bytes_l / (ms_l * 1e-3) / 1e9,
+            "frac_of_hbm": bytes_l / (ms_l * 1e-3) / 1e9 / PEAK_HBM_GBS}
+        del kl, vl
 
     if not args.no_cpu_baseline:
         import oracle
