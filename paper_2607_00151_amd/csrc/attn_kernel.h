@@ -96,7 +96,7 @@ __device__ __forceinline__ bf16x4 lds_read_tr(const lds_u8* p) {
 __device__ __forceinline__ float pair_max(float x) {
   // lanes l and l ^ 32 exchange; both halves see the same pair
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
 __device__ __forceinline__ float pair_sum(float x) {
@@ -303,7 +303,7 @@ __global__ __launch_bounds__(64 * WAVES, (QT == 1 ? 2 : 1)) void attn_kernel(Att
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt][qt][e]);
+          for (int e = 0; e < 16; ++e) mx = vmax(mx, s[kt][qt][e]);
         mx = pair_max(mx);
         const float cand = mx * a.c;
         if (__ballot(cand > m_used[qt] + kRescaleLog2)) {

@@ -1,0 +1,454 @@
+// Software-pipelined form of the paged prefill attention (same work items,
+// same LDS tiles and operand layouts as attn_kernel<P, 1, 4>).
+//
+// A CDNA4 SIMD overlaps matrix-core and VALU work only when both come from
+// the same wave: an MFMA-only wave next to a VALU-only wave on one SIMD runs
+// no faster than the two back to back, while a few VALU ops placed after each
+// 32x32x16 MFMA of one wave cost little beyond the MFMA time (measured on
+// MI355X).  So each wave splits key tile t into two interleaved phases,
+//   phase 1:  S(t+1)^T = K(t+1) Q^T   16 MFMAs
+//             P(t) = exp2(c S(t) - m) VALU (32 fma, 32 exp, 16 cvt, 32 add
+//                                       per lane; the adds form l)
+//   phase 2:  O^T += V(t)^T P(t)^T    16 MFMAs
+//             row max of S(t+1) and the lazy rescale test
+// with K one tile ahead of V.  The VALU work of each phase depends only on
+// results of the previous phase, so it issues between the MFMAs.  Steps whose
+// next tile needs the causal mask, and the last step, run the same sequence
+// without the interleaving.
+#pragma once
+
+#include "attn_kernel.h"
+
+namespace sa {
+
+
+template <int N>
+struct IntC {
+  static constexpr int value = N;
+};
+
+// kPoolRsrc: a layer's K (and V) pool spans < 2^31 bytes, so one buffer
+// resource per pool reaches every page through the 32-bit scalar offset;
+// otherwise each page load builds a resource for its page.
+template <int P, bool kPoolRsrc>
+__global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
+  static_assert(P == 16 || P == 32, "page size");
+  constexpr int WAVES = 4;
+  constexpr int kRows = 32 * WAVES;                        // rows per item
+  constexpr int kTileBytes = kKT * kHD * 2;                // 16 KB
+  constexpr int kPagesPerTile = kKT / P;
+  constexpr int kNJ = 16 / WAVES;                          // loads per wave per tile and operand
+  constexpr int kAhead = 2;                                // operand reads issued this many steps ahead
+  __shared__ __attribute__((aligned(1024))) uint8_t k_lds0[kTileBytes], k_lds1[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t v_lds0[kTileBytes], v_lds1[kTileBytes];
+
+  const AttnItem it = ld_uniform(a.items + blockIdx.x);
+  if (it.kv_begin >= it.kv_end) return;                     // padding item
+  const SeqDesc sd = ld_uniform(a.seqs + it.seq);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & (WAVES - 1);
+  const int hh = lane >> 5;
+  const int G = a.G;
+  const int rows_total = sd.q_len * G;
+  const int pre = sd.kv_len - sd.q_len;
+
+  const int r_row = it.row0 + wave * 32 + (lane & 31);
+  const bool row_valid = r_row < rows_total;
+  const int rr = row_valid ? r_row : rows_total - 1;
+  const int tok = rr / G;
+  const int head = it.kvh * G + (rr - tok * G);
+  const int qpos = pre + tok;
+
+  const int wrow0 = it.row0 + wave * 32;
+  const bool wave_active = wrow0 < rows_total;
+  const int w_full = min(it.kv_end, pre + wrow0 / G + 1);    // keys below are visible to all rows
+
+  bf16x8 qop[8];
+  {
+    const uint16_t* qrow = a.q + ((int64_t)(sd.q_start + tok) * a.Hq + head) * kHD;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) qop[ks] = ld_bf16x8(qrow + (2 * ks + hh) * 8);
+  }
+
+  const int32_t pt_base = ld_uniform(a.indptr + it.seq);
+  const int32_t pt_count = ld_uniform(a.indptr + it.seq + 1) - pt_base;
+  const int64_t slot_bytes = (int64_t)a.Hkv * P * kHD * 2;
+  const char* kbase = (const char*)a.k;
+  const char* vbase = (const char*)a.v;
+  int koff[kNJ], voff[kNJ];
+#pragma unroll
+  for (int j = 0; j < kNJ; ++j) {
+    const int key = 4 * (j * WAVES + wave) + (lane >> 4);
+    const int row_bytes = (it.kvh * P + key % P) * (kHD * 2);
+    koff[j] = row_bytes + (((lane & 15) ^ swz_k(key)) << 4);
+    voff[j] = row_bytes + (((lane & 15) ^ swz_v(key)) << 4);
+  }
+
+  struct Slots {
+    int32_t s[kPagesPerTile];
+  };
+  auto fetch = [&](int t) __attribute__((always_inline)) {
+    Slots S;
+#pragma unroll
+    for (int j = 0; j < kPagesPerTile; ++j) {
+      const int pg = t * kPagesPerTile + j;
+      S.s[j] = (pg >= 0 && pg < pt_count) ? ld_uniform(a.indices + pt_base + pg) : -1;
+    }
+    return S;
+  };
+  auto slot_ok = [&](int32_t s) __attribute__((always_inline)) { return s >= 0 && s < a.num_slots; };
+
+  const int t0 = it.kv_begin / kKT;
+  const int t1 = (it.kv_end + kKT - 1) / kKT;
+
+  // The item's page slots are checked once: a block whose table is intact
+  // (every page its keys need present and in range) loads tiles without
+  // per-page tests; otherwise every tile takes the checked path, which
+  // zero-fills what it cannot load and raises the error flag.
+  bool table_bad = pt_count < (it.kv_end + P - 1) / P;
+  for (int pg = t0 * kPagesPerTile + tid; pg < min(t1 * kPagesPerTile, pt_count); pg += kRows * 2)
+    table_bad |= !slot_ok(a.indices[pt_base + pg]);
+  const bool table_ok = !__syncthreads_or(table_bad);
+  const uint32_t pool_bytes = kPoolRsrc ? (uint32_t)(a.num_slots * slot_bytes) : 0u;
+  const __amdgpu_buffer_rsrc_t rsrc_k =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.k), (short)0, (int)pool_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsrc_v =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.v), (short)0, (int)pool_bytes, 0x00020000);
+
+  // global -> LDS loads of one operand (K or V) of tile t into dst
+  auto load_op = [&](int t, const Slots& S, const char* base, const __amdgpu_buffer_rsrc_t& rsrc, const int* off,
+                     lds_u8* dst) __attribute__((always_inline)) {
+    const int ts = t * kKT;
+    if (table_ok && ts + kKT <= it.kv_end) {
+#pragma unroll
+      for (int j = 0; j < kNJ; ++j) {
+        const int gb = j * WAVES + wave;
+        const int32_t slot = S.s[(4 * gb) / P];
+        __attribute__((address_space(3))) void* d = (__attribute__((address_space(3))) void*)(dst + gb * 1024);
+        if constexpr (kPoolRsrc)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, d, 16, off[j], (uint32_t)slot * (uint32_t)slot_bytes, 0, 0);
+        else
+          lds_dma16(base + (int64_t)slot * slot_bytes, (uint32_t)slot_bytes, off[j], d);
+      }
+    } else {
+      bool bad = false;
+#pragma unroll
+      for (int j = 0; j < kNJ; ++j) {
+        const int gb = j * WAVES + wave;
+        const int32_t s = S.s[(4 * gb) / P];
+        const bool page_needed = ts + 4 * gb < it.kv_end;
+        bad |= page_needed && !slot_ok(s);
+        const bool ld = page_needed && slot_ok(s) && ts + 4 * gb + (lane >> 4) < it.kv_end;
+        if (ld) {
+          lds_dma16(base + (int64_t)s * slot_bytes, (uint32_t)slot_bytes, off[j],
+                    (__attribute__((address_space(3))) void*)(dst + gb * 1024));
+        } else {
+          // absent keys: zero rows keep the masked products finite
+          const u32x4 z = {0u, 0u, 0u, 0u};
+          *(__attribute__((address_space(3))) u32x4*)(dst + gb * 1024 + lane * 16) = z;
+        }
+      }
+      if (bad && lane == 0) atomicOr(a.err, 1);
+    }
+  };
+
+  f32x16 oacc[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) oacc[dt] = f32x16{};
+  float m_used = -INFINITY;  // exponent offset in use (log2 domain)
+  float msub = 0.f;          // m_used, or 0 while it is -inf
+  float l = 0.f;             // this lane's share of the denominator
+  f32x16 sc[2][2];           // [buffer][32-key block] scores of tiles t and t + 1
+  bf16x8 pop[4];             // [16-key group] probabilities of tile t
+
+  const int krow = lane & 31;
+  const int tr_g = lane >> 4, tr_s = lane & 15;
+  const int tr_key = 4 * (tr_g >> 1) + (tr_s >> 2);
+  const int tr_d = 16 * (tr_g & 1) + 4 * (tr_s & 3);
+
+  // MFMA operands from LDS.  S step i: 32-key block i & 1, d-chunk pair
+  // i >> 1 (the two accumulation chains alternate).  PV step i: 16-key group
+  // i >> 2, 32-wide d block i & 3.
+  auto read_k = [&](const lds_u8* kb, int i) __attribute__((always_inline)) {
+    const int key = 32 * (i & 1) + krow;
+    return *(const __attribute__((address_space(3))) bf16x8*)(
+        kb + key * 256 + (((2 * (i >> 1) + hh) ^ swz_k(key)) << 4));
+  };
+  auto read_v = [&](const lds_u8* vb, int i) __attribute__((always_inline)) {
+    bf16x8 vop;
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int vkey = 16 * (i >> 2) + 8 * r + tr_key;
+      const int d = 32 * (i & 3) + tr_d;
+      const bf16x4 x = lds_read_tr(vb + vkey * 256 + ((((d >> 3) ^ swz_v(vkey)) << 4) | ((d & 7) << 1)));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) vop[4 * r + e] = x[e];
+    }
+    return vop;
+  };
+  auto s_step = [&](f32x16* S, bf16x8 kop, int i) __attribute__((always_inline)) {
+    S[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[i >> 1], i < 2 ? f32x16{} : S[i & 1], 0, 0, 0);
+  };
+  auto pv_step = [&](bf16x8 vop, int i) __attribute__((always_inline)) {
+    oacc[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[i >> 2], oacc[i & 3], 0, 0, 0);
+  };
+  // probabilities of score pair j (elements 2j, 2j + 1 of the tile, in P^T
+  // slot order: group j >> 2, slots 2 (j & 3) and 2 (j & 3) + 1)
+  auto exp_pair = [&](const f32x16* S, int j) __attribute__((always_inline)) {
+    const int g = j >> 2, e = 2 * (j & 3);
+    const float p0 = exp2f_fast(__builtin_fmaf(S[g >> 1][8 * (g & 1) + e], a.c, -msub));
+    const float p1 = exp2f_fast(__builtin_fmaf(S[g >> 1][8 * (g & 1) + e + 1], a.c, -msub));
+    pop[g][e] = (__bf16)p0;
+    pop[g][e + 1] = (__bf16)p1;
+    return p0 + p1;
+  };
+  auto mask_tile = [&](int t, f32x16* S) __attribute__((always_inline)) {
+    const int ts = t * kKT;
+    const int lim = min(qpos, it.kv_end - 1);
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int key = ts + 32 * kt + 8 * (e >> 2) + 4 * hh + (e & 3);
+        if (key > lim) S[kt][e] = -INFINITY;
+      }
+  };
+  // lazy rescale: move the offset when the row max outgrows it by 2^kRescaleLog2
+  auto rescale_test = [&](float mx) __attribute__((always_inline)) {
+    mx = pair_max(mx);
+    const float cand = mx * a.c;
+    if (__ballot(cand > m_used + kRescaleLog2)) {
+      const float m_new = fmaxf(m_used, cand);
+      const float alpha = (m_new == -INFINITY) ? 1.f : exp2f_fast(m_used - m_new);
+      m_used = m_new;
+      msub = (m_used == -INFINITY) ? 0.f : m_used;
+      l *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) oacc[dt][e] *= alpha;
+    }
+  };
+  auto row_max = [&](const f32x16* S) __attribute__((always_inline)) {
+    float mx = S[0][0];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mx = vmax(mx, S[kt][e]);
+    return mx;
+  };
+
+  // plain step, S(t) in sc[0]: S(t+1) into sc[1] if there is a next tile;
+  // P(t); O += V(t) P(t); sum; mask and rescale test of tile t+1, which then
+  // moves to sc[0]
+  auto plain_step = [&](int t, const lds_u8* kb, const lds_u8* vb) __attribute__((always_inline)) {
+    const bool has_next = t + 1 < t1;
+    if (has_next) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) s_step(sc[1], read_k(kb, i), i);
+    }
+    float ls = 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) ls += exp_pair(sc[0], j);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) pv_step(read_v(vb, i), i);
+    l += ls;
+    if (has_next) {
+      if ((t + 2) * kKT > w_full) mask_tile(t + 1, sc[1]);
+      rescale_test(row_max(sc[1]));
+      sc[0][0] = sc[1][0];
+      sc[0][1] = sc[1][1];
+    }
+  };
+
+  // interleaved step (next tile exists and needs no mask)
+  Slots s_a, s_b;          // pages of tiles t + 1 and t + 2 in step t
+
+  // one 16-byte-per-lane page load of a full tile with an intact table
+  auto tile_load = [&](const Slots& S, const char* base, const __amdgpu_buffer_rsrc_t& rsrc, const int* off,
+                       lds_u8* dst, int j) __attribute__((always_inline)) {
+    const int gb = j * WAVES + wave;
+    const int32_t slot = S.s[(4 * gb) / P];
+    __attribute__((address_space(3))) void* d = (__attribute__((address_space(3))) void*)(dst + gb * 1024);
+    if constexpr (kPoolRsrc)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, d, 16, off[j], (uint32_t)slot * (uint32_t)slot_bytes, 0, 0);
+    else
+      lds_dma16(base + (int64_t)slot * slot_bytes, (uint32_t)slot_bytes, off[j], d);
+  };
+
+  // interleaved step; also issues this step's loads, K(t+2) into kn and
+  // V(t+1) into vn (full tiles, intact table), one per MFMA of phase 1
+  auto fast_step = [&](auto bc, const lds_u8* kb, const lds_u8* vb, lds_u8* kn, lds_u8* vn) __attribute__((always_inline)) {
+    constexpr int B = decltype(bc)::value, N = 1 - B;
+    bf16x8 kop[16], vop[16];
+    // phase 1: S(t+1) MFMAs, P(t) between them.  The exponentials run as a
+    // three-stage pipeline over score pairs (fma of pair i+2, exp of pair
+    // i+1, bf16 pack of pair i in step i), so no VALU op waits on the one
+    // before it and the next MFMA issues on time.
+    float xs[16][2], ex[16][2];
+    float ls[2] = {0.f, 0.f};   // two accumulation chains for the denominator
+    auto arg = [&](int j, int h) __attribute__((always_inline)) {
+      const int g = j >> 2, e = 2 * (j & 3) + h;
+      return __builtin_fmaf(sc[B][g >> 1][8 * (g & 1) + e], a.c, -msub);
+    };
+#pragma unroll
+    for (int i = 0; i < kAhead; ++i) kop[i] = read_k(kb, i);
+    xs[0][0] = arg(0, 0);
+    xs[0][1] = arg(0, 1);
+    xs[1][0] = arg(1, 0);
+    xs[1][1] = arg(1, 1);
+    ex[0][0] = exp2f_fast(xs[0][0]);
+    ex[0][1] = exp2f_fast(xs[0][1]);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      if (i + kAhead < 16) kop[i + kAhead] = read_k(kb, i + kAhead);
+      if (i < kNJ) tile_load(s_b, kbase, rsrc_k, koff, kn, i);
+      else if (i < 2 * kNJ) tile_load(s_a, vbase, rsrc_v, voff, vn, i - kNJ);
+      s_step(sc[N], kop[i], i);
+      if (i + 2 < 16) {
+        xs[i + 2][0] = arg(i + 2, 0);
+        xs[i + 2][1] = arg(i + 2, 1);
+      }
+      if (i + 1 < 16) {
+        ex[i + 1][0] = exp2f_fast(xs[i + 1][0]);
+        ex[i + 1][1] = exp2f_fast(xs[i + 1][1]);
+      }
+      ls[i & 1] += ex[i][0] + ex[i][1];
+      pop[i >> 2][2 * (i & 3)] = (__bf16)ex[i][0];
+      pop[i >> 2][2 * (i & 3) + 1] = (__bf16)ex[i][1];
+      // pin each step's operand read, tile load, MFMA and VALU work to this step
+      if (i + kAhead < 16) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if (i < 2 * kNJ) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // phase 2: PV MFMAs; sum of P(t) and row max of S(t+1) between them
+#pragma unroll
+    for (int i = 0; i < kAhead; ++i) vop[i] = read_v(vb, i);
+    // two accumulation chains for the row max
+    float mx[2] = {-INFINITY, -INFINITY};
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      if (i + kAhead < 16) vop[i + kAhead] = read_v(vb, i + kAhead);
+      pv_step(vop[i], i);
+      mx[i & 1] = vmax(mx[i & 1], vmax(sc[N][i & 1][2 * (i >> 1)], sc[N][i & 1][2 * (i >> 1) + 1]));
+      if (i + kAhead < 16) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    l += ls[0] + ls[1];
+    rescale_test(vmax(mx[0], mx[1]));
+  };
+
+  lds_u8* const K0 = (lds_u8*)k_lds0;
+  lds_u8* const K1 = (lds_u8*)k_lds1;
+  lds_u8* const V0 = (lds_u8*)v_lds0;
+  lds_u8* const V1 = (lds_u8*)v_lds1;
+
+  // ---- prologue: K(t0), V(t0), K(t0 + 1); S(t0) and its rescale test
+  {
+    const Slots s0 = fetch(t0);
+    load_op(t0, s0, kbase, rsrc_k, koff, K0);
+    load_op(t0, s0, vbase, rsrc_v, voff, V0);
+  }
+  s_a = fetch(t0 + 1);
+  if (t0 + 1 < t1) load_op(t0 + 1, s_a, kbase, rsrc_k, koff, K1);
+  s_b = fetch(t0 + 2);
+  __builtin_amdgcn_s_waitcnt(0x0070);
+  lds_barrier();
+  if (wave_active) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s_step(sc[0], read_k(K0, i), i);
+    if ((t0 + 1) * kKT > w_full) mask_tile(t0, sc[0]);
+    rescale_test(row_max(sc[0]));
+  }
+
+  // ---- step t reads K(t+1) and V(t) and loads K(t+2), V(t+1).  K(t) and
+  // V(t) sit in buffer (t - t0) & 1.
+  auto wait_tiles = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(0x0070);                     // my loads of K(t+1), V(t) landed
+    lds_barrier();                                          // everyone's; the next buffers are free
+  };
+  auto top = [&](int t, lds_u8* kn, lds_u8* vn) __attribute__((always_inline)) {
+    wait_tiles();
+    if (t + 2 < t1) load_op(t + 2, s_b, kbase, rsrc_k, koff, kn);
+    if (t + 1 < t1) load_op(t + 1, s_a, vbase, rsrc_v, voff, vn);
+  };
+  auto advance = [&](int t) __attribute__((always_inline)) {
+    s_a = s_b;
+    s_b = fetch(t + 3);
+  };
+  // Steps t < t_fast interleave: their next tile needs no mask and the
+  // tiles they load, K(t+2) and V(t+1), are full and covered by an intact
+  // table.  Waves run different numbers of each kind of step but the same
+  // number of steps, each with one barrier and its share of the tile loads.
+  const int t_fast = (wave_active && table_ok)
+                         ? max(t0, min(min(t1 - 1, w_full / kKT - 1), it.kv_end / kKT - 2))
+                         : t0;
+  int t = t0;
+  for (; t + 1 < t_fast; t += 2) {
+    wait_tiles();
+    fast_step(IntC<0>{}, K1, V0, K0, V1);
+    advance(t);
+    wait_tiles();
+    fast_step(IntC<1>{}, K0, V1, K1, V0);
+    advance(t + 1);
+  }
+  if (t < t_fast) {
+    wait_tiles();
+    fast_step(IntC<0>{}, K1, V0, K0, V1);
+    advance(t);
+    ++t;
+  }
+  if ((t - t0) & 1) {                                       // S(t) is in sc[1]
+    sc[0][0] = sc[1][0];
+    sc[0][1] = sc[1][1];
+  }
+  for (; t < t1; ++t) {
+    const bool odd = (t - t0) & 1;
+    top(t, odd ? K1 : K0, odd ? V0 : V1);
+    if (wave_active) plain_step(t, odd ? K0 : K1, odd ? V1 : V0);
+    advance(t);
+  }
+
+  if (!wave_active) return;
+  const float l_tot = pair_sum(l);
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  const float lse2 = l_tot > 0.f ? m_used + __builtin_amdgcn_logf(l_tot) : -INFINITY;
+  if (it.part < 0) {
+    if (row_valid) {
+      uint16_t* orow = a.o + ((int64_t)(sd.q_start + tok) * a.Hq + head) * kHD;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int d = 32 * dt + 8 * i + 4 * hh;
+          st_bf16x4(orow + d, oacc[dt][4 * i] * inv, oacc[dt][4 * i + 1] * inv,
+                    oacc[dt][4 * i + 2] * inv, oacc[dt][4 * i + 3] * inv);
+        }
+      if (a.lse != nullptr && hh == 0)
+        a.lse[(int64_t)(sd.q_start + tok) * a.Hq + head] = lse2 * 0.69314718055994531f;
+    }
+  } else {
+    const int lrow = wave * 32 + (lane & 31);
+    float* po = a.part_o + ((int64_t)it.part * kRows + lrow) * kHD;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int d = 32 * dt + 8 * i + 4 * hh;
+        f32x4 w = {oacc[dt][4 * i] * inv, oacc[dt][4 * i + 1] * inv, oacc[dt][4 * i + 2] * inv,
+                   oacc[dt][4 * i + 3] * inv};
+        *(f32x4*)(po + d) = w;
+      }
+    if (hh == 0) a.part_lse[(int64_t)it.part * kRows + lrow] = lse2;
+  }
+}
+
+}  // namespace sa

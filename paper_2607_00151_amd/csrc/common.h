@@ -31,6 +31,35 @@ __device__ __forceinline__ T ld_uniform(const T* p) {
   return out;
 }
 
+// Workgroup barrier that orders LDS accesses only.  __syncthreads() also
+// waits for every outstanding global access (vmcnt(0)), which would drain
+// the direct-to-LDS tile loads a kernel deliberately keeps in flight across
+// the barrier; their completion is awaited explicitly where it is needed.
+// The empty asm statements keep the compiler from moving memory accesses
+// across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): my LDS accesses are done
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// 16-byte global -> LDS copy through a buffer resource covering
+// [base, base + nbytes): lane i of the wave fills dst + 16 i with the 16 bytes
+// at base + voff (zeros if voff is outside the range).  The buffer form keeps
+// the compiler's LDS wait counting exact while the copy is in flight (the
+// global-segment form makes it wait for every outstanding LDS access).
+__device__ __forceinline__ void lds_dma16(const void* base, uint32_t nbytes, uint32_t voff,
+                                          __attribute__((address_space(3))) void* dst) {
+  const __amdgpu_buffer_rsrc_t r =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)nbytes, 0x00020000);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, 0, 0, 0);
+}
+
+// max that propagates NaN instead of quieting it: lowers to v_maximum3_f32
+// without the canonicalising v_max x, x that fmaxf needs for MFMA results
+__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
 // v_exp_f32: 2^x (exp2(-inf) = 0).
 __device__ __forceinline__ float exp2f_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 

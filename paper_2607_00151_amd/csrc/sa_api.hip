@@ -14,6 +14,7 @@
 
 #include "sa.h"
 #include "attn_kernel.h"
+#include "attn_pipe.h"
 #include "kv_kernels.h"
 
 namespace {
@@ -156,12 +157,13 @@ sa_status check_ctx(sa_ctx* ctx) {
 }
 
 // Attention kernel variants: 32 * qt query rows per wave, `waves` waves per
-// work item.  SA_ATTN_VARIANT overrides the default (tuning only).
+// work item; `pipe` selects the software-pipelined kernel.  SA_ATTN_VARIANT
+// overrides the default (tuning only).
 struct AttnVariant {
-  int qt, waves;
+  int qt, waves, pipe;
 };
-constexpr AttnVariant kVariants[] = {{1, 4}, {2, 2}, {2, 4}};
-constexpr int kDefaultVariant = 0;
+constexpr AttnVariant kVariants[] = {{1, 4, 0}, {2, 2, 0}, {2, 4, 0}, {1, 4, 1}};
+constexpr int kDefaultVariant = 3;
 
 AttnVariant attn_variant() {
   static int v = [] {
@@ -173,8 +175,12 @@ AttnVariant attn_variant() {
 }
 
 template <int P>
-void launch_attn_p(AttnVariant v, dim3 grid, hipStream_t st, const sa::AttnArgs& a) {
-  if (v.qt == 1 && v.waves == 4)
+void launch_attn_p(AttnVariant v, bool pool_rsrc, dim3 grid, hipStream_t st, const sa::AttnArgs& a) {
+  if (v.pipe && pool_rsrc)
+    hipLaunchKernelGGL((sa::attn_pipe_kernel<P, true>), grid, dim3(256), 0, st, a);
+  else if (v.pipe)
+    hipLaunchKernelGGL((sa::attn_pipe_kernel<P, false>), grid, dim3(256), 0, st, a);
+  else if (v.qt == 1 && v.waves == 4)
     hipLaunchKernelGGL((sa::attn_kernel<P, 1, 4>), grid, dim3(256), 0, st, a);
   else if (v.qt == 2 && v.waves == 2)
     hipLaunchKernelGGL((sa::attn_kernel<P, 2, 2>), grid, dim3(128), 0, st, a);
@@ -182,9 +188,11 @@ void launch_attn_p(AttnVariant v, dim3 grid, hipStream_t st, const sa::AttnArgs&
     hipLaunchKernelGGL((sa::attn_kernel<P, 2, 4>), grid, dim3(256), 0, st, a);
 }
 
-void launch_attn(int page_size, AttnVariant v, dim3 grid, hipStream_t st, const sa::AttnArgs& a) {
-  if (page_size == 16) launch_attn_p<16>(v, grid, st, a);
-  else launch_attn_p<32>(v, grid, st, a);
+// pool_rsrc: a layer's K (and V) pool spans < 2^31 bytes, so one buffer
+// resource per pool addresses every page with a 32-bit offset
+void launch_attn(int page_size, AttnVariant v, bool pool_rsrc, dim3 grid, hipStream_t st, const sa::AttnArgs& a) {
+  if (page_size == 16) launch_attn_p<16>(v, pool_rsrc, grid, st, a);
+  else launch_attn_p<32>(v, pool_rsrc, grid, st, a);
 }
 
 }  // namespace
@@ -570,7 +578,8 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
   a.Hkv = Hkv;
   a.G = G;
   a.c = softmax_scale * 1.4426950408889634f;
-  launch_attn(layout->page_size, var, dim3((unsigned)items.size()), (hipStream_t)stream, a);
+  const bool pool_rsrc = layer_elems(layout) * 2 < ((int64_t)1 << 31);
+  launch_attn(layout->page_size, var, pool_rsrc, dim3((unsigned)items.size()), (hipStream_t)stream, a);
   SA_HIP(hipGetLastError());
   if (!groups.empty()) {
     sa::MergeArgs m{};
