@@ -524,10 +524,18 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
   for (const Work& w : work) load[w.xcd] += w.tiles;
   const int64_t mx = *std::max_element(load, load + kNumXcd);
   const int64_t mn = *std::min_element(load, load + kNumXcd);
+  // Two blocks share a CU, and with a grid of at most two rounds the
+  // dispatcher pairs block i with block i + (number of CUs) (measured): the
+  // second round is reversed so the longest items share CUs with the
+  // shortest and every CU gets about the same work.
+  auto pair_rounds = [](std::vector<sa::AttnItem>& q, size_t first_round) {
+    if (q.size() > first_round && q.size() <= 2 * first_round) std::reverse(q.begin() + first_round, q.end());
+  };
   std::vector<sa::AttnItem> items;
   if (mx > 0 && (double)(mx - mn) <= 0.1 * (double)mx) {
     std::vector<std::vector<sa::AttnItem>> queue(kNumXcd);
     for (const Work& w : work) queue[w.xcd].push_back(w.it);
+    for (auto& qd : queue) pair_rounds(qd, (size_t)std::max(1, ctx->num_cu / kNumXcd));
     size_t depth = 0;
     for (auto& qd : queue) depth = std::max(depth, qd.size());
     items.assign(depth * kNumXcd, sa::AttnItem{0, 0, 0, 0, 0, -1});
@@ -535,6 +543,7 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
       for (size_t i = 0; i < queue[x].size(); ++i) items[i * kNumXcd + x] = queue[x][i];
   } else {
     for (const Work& w : work) items.push_back(w.it);
+    pair_rounds(items, (size_t)ctx->num_cu);
   }
 
   if (n_parts > 0) {
