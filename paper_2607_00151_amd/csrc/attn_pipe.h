@@ -357,9 +357,21 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
     load_op(t0, s0, kbase, rsrc_k, koff, K0);
     load_op(t0, s0, vbase, rsrc_v, voff, V0);
   }
-  s_a = fetch(t0 + 1);
-  if (t0 + 1 < t1) load_op(t0 + 1, s_a, kbase, rsrc_k, koff, K1);
-  s_b = fetch(t0 + 2);
+  s_b = fetch(t0 + 1);
+  if (t0 + 1 < t1) load_op(t0 + 1, s_b, kbase, rsrc_k, koff, K1);
+  // Interleaved steps take the page slots of their loads from a vector load
+  // issued a step ahead: it is counted with the tile loads and has a whole
+  // step to land, where a scalar load would be waited for at the next barrier.
+  const __amdgpu_buffer_rsrc_t rsrc_pt = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int32_t*>(a.indices + pt_base), (short)0, pt_count * 4, 0x00020000);
+  typedef uint32_t slot_vec __attribute__((ext_vector_type(kPagesPerTile)));
+  auto fetch_vec = [&](int t) __attribute__((always_inline)) {
+    if constexpr (kPagesPerTile == 4)
+      return __builtin_bit_cast(slot_vec, __builtin_amdgcn_raw_buffer_load_b128(rsrc_pt, t * 16, 0, 0));
+    else
+      return __builtin_bit_cast(slot_vec, __builtin_amdgcn_raw_buffer_load_b64(rsrc_pt, t * 8, 0, 0));
+  };
+  slot_vec v_next = fetch_vec(t0 + 2);                      // pages of tile t + 2, in flight
   __builtin_amdgcn_s_waitcnt(0x0070);
   lds_barrier();
   if (wave_active) {
@@ -384,6 +396,14 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
     s_a = s_b;
     s_b = fetch(t + 3);
   };
+  // start of interleaved step t: s_a <- pages of t + 1, s_b <- pages of t + 2
+  // (landed with the last tile loads), pages of t + 3 requested
+  auto advance_fast = [&](int t) __attribute__((always_inline)) {
+    s_a = s_b;
+#pragma unroll
+    for (int j = 0; j < kPagesPerTile; ++j) s_b.s[j] = (int32_t)__builtin_amdgcn_readfirstlane(v_next[j]);
+    v_next = fetch_vec(t + 3);
+  };
   // Steps t < t_fast interleave: their next tile needs no mask and the
   // tiles they load, K(t+2) and V(t+1), are full and covered by an intact
   // table.  Waves run different numbers of each kind of step but the same
@@ -394,18 +414,21 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   int t = t0;
   for (; t + 1 < t_fast; t += 2) {
     wait_tiles();
+    advance_fast(t);
     fast_step(IntC<0>{}, K1, V0, K0, V1);
-    advance(t);
     wait_tiles();
+    advance_fast(t + 1);
     fast_step(IntC<1>{}, K0, V1, K1, V0);
-    advance(t + 1);
   }
   if (t < t_fast) {
     wait_tiles();
+    advance_fast(t);
     fast_step(IntC<0>{}, K1, V0, K0, V1);
-    advance(t);
     ++t;
   }
+  // plain steps: scalar page reads (-1 for pages the table lacks)
+  s_a = fetch(t + 1);
+  s_b = fetch(t + 2);
   if ((t - t0) & 1) {                                       // S(t) is in sc[1]
     sc[0][0] = sc[1][0];
     sc[0][1] = sc[1][1];
