@@ -7,10 +7,11 @@
 // 32x32x16 MFMA of one wave cost little beyond the MFMA time (measured on
 // MI355X).  So each wave splits key tile t into two interleaved phases,
 //   phase 1:  S(t+1)^T = K(t+1) Q^T   16 MFMAs
-//             P(t) = exp2(c S(t) - m) VALU (32 fma, 32 exp, 16 cvt, 32 add
-//                                       per lane; the adds form l)
+//             P(t) = exp2(x(t))       VALU (32 exp, 16 cvt, 32 add per lane;
+//                                       the adds form l)
 //   phase 2:  O^T += V(t)^T P(t)^T    16 MFMAs
-//             row max of S(t+1) and the lazy rescale test
+//             x(t+1) = c S(t+1) - m   VALU (32 fma), its row max and the
+//                                       lazy rescale test
 // with K one tile ahead of V.  The VALU work of each phase depends only on
 // results of the previous phase, so it issues between the MFMAs.  Steps whose
 // next tile needs the causal mask, and the last step, run the same sequence
@@ -194,12 +195,24 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   auto pv_step = [&](bf16x8 vop, int i) __attribute__((always_inline)) {
     oacc[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[i >> 2], oacc[i & 3], 0, 0, 0);
   };
-  // probabilities of score pair j (elements 2j, 2j + 1 of the tile, in P^T
-  // slot order: group j >> 2, slots 2 (j & 3) and 2 (j & 3) + 1)
-  auto exp_pair = [&](const f32x16* S, int j) __attribute__((always_inline)) {
+  // A tile's scores are rewritten in place as x = c s - msub, the exponent of
+  // their probability against the offset in use.
+  auto to_x = [&](f32x16* S) __attribute__((always_inline)) {
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) S[kt][e] = __builtin_fmaf(S[kt][e], a.c, -msub);
+  };
+  // probabilities of pair j (elements 2j, 2j + 1 of the tile, in P^T slot
+  // order: group j >> 2, slots 2 (j & 3) and 2 (j & 3) + 1)
+  auto xpair = [&](const f32x16* X, int j, int h) __attribute__((always_inline)) {
+    const int g = j >> 2;
+    return X[g >> 1][8 * (g & 1) + 2 * (j & 3) + h];
+  };
+  auto exp_pair = [&](const f32x16* X, int j) __attribute__((always_inline)) {
     const int g = j >> 2, e = 2 * (j & 3);
-    const float p0 = exp2f_fast(__builtin_fmaf(S[g >> 1][8 * (g & 1) + e], a.c, -msub));
-    const float p1 = exp2f_fast(__builtin_fmaf(S[g >> 1][8 * (g & 1) + e + 1], a.c, -msub));
+    const float p0 = exp2f_fast(xpair(X, j, 0));
+    const float p1 = exp2f_fast(xpair(X, j, 1));
     pop[g][e] = (__bf16)p0;
     pop[g][e + 1] = (__bf16)p1;
     return p0 + p1;
@@ -215,20 +228,28 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
         if (key > lim) S[kt][e] = -INFINITY;
       }
   };
-  // lazy rescale: move the offset when the row max outgrows it by 2^kRescaleLog2
-  auto rescale_test = [&](float mx) __attribute__((always_inline)) {
+  // lazy rescale, given the row max mx of a tile's x values: move the offset
+  // when c (row max) outgrows it by 2^kRescaleLog2, rescale O and l, and
+  // shift the tile's x values to the new offset
+  auto rescale_test = [&](float mx, f32x16* X) __attribute__((always_inline)) {
     mx = pair_max(mx);
-    const float cand = mx * a.c;
+    const float cand = mx + msub;                           // c * row max
     if (__ballot(cand > m_used + kRescaleLog2)) {
       const float m_new = fmaxf(m_used, cand);
       const float alpha = (m_new == -INFINITY) ? 1.f : exp2f_fast(m_used - m_new);
       m_used = m_new;
-      msub = (m_used == -INFINITY) ? 0.f : m_used;
+      const float msub_new = (m_used == -INFINITY) ? 0.f : m_used;
+      const float shift = msub_new - msub;
+      msub = msub_new;
       l *= alpha;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
         for (int e = 0; e < 16; ++e) oacc[dt][e] *= alpha;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) X[kt][e] -= shift;
     }
   };
   auto row_max = [&](const f32x16* S) __attribute__((always_inline)) {
@@ -256,8 +277,9 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
     for (int i = 0; i < 16; ++i) pv_step(read_v(vb, i), i);
     l += ls;
     if (has_next) {
+      to_x(sc[1]);
       if ((t + 2) * kKT > w_full) mask_tile(t + 1, sc[1]);
-      rescale_test(row_max(sc[1]));
+      rescale_test(row_max(sc[1]), sc[1]);
       sc[0][0] = sc[1][0];
       sc[0][1] = sc[1][1];
     }
@@ -283,37 +305,24 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   auto fast_step = [&](auto bc, const lds_u8* kb, const lds_u8* vb, lds_u8* kn, lds_u8* vn) __attribute__((always_inline)) {
     constexpr int B = decltype(bc)::value, N = 1 - B;
     bf16x8 kop[16], vop[16];
-    // phase 1: S(t+1) MFMAs, P(t) between them.  The exponentials run as a
-    // three-stage pipeline over score pairs (fma of pair i+2, exp of pair
-    // i+1, bf16 pack of pair i in step i), so no VALU op waits on the one
-    // before it and the next MFMA issues on time.
-    float xs[16][2], ex[16][2];
+    // phase 1: S(t+1) MFMAs, P(t) between them: the exponentials of pair
+    // i+1 and the bf16 pack and sum of pair i in step i, so no VALU op waits
+    // on the one before it and the next MFMA issues on time.
+    float ex[16][2];
     float ls[2] = {0.f, 0.f};   // two accumulation chains for the denominator
-    auto arg = [&](int j, int h) __attribute__((always_inline)) {
-      const int g = j >> 2, e = 2 * (j & 3) + h;
-      return __builtin_fmaf(sc[B][g >> 1][8 * (g & 1) + e], a.c, -msub);
-    };
 #pragma unroll
     for (int i = 0; i < kAhead; ++i) kop[i] = read_k(kb, i);
-    xs[0][0] = arg(0, 0);
-    xs[0][1] = arg(0, 1);
-    xs[1][0] = arg(1, 0);
-    xs[1][1] = arg(1, 1);
-    ex[0][0] = exp2f_fast(xs[0][0]);
-    ex[0][1] = exp2f_fast(xs[0][1]);
+    ex[0][0] = exp2f_fast(xpair(sc[B], 0, 0));
+    ex[0][1] = exp2f_fast(xpair(sc[B], 0, 1));
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       if (i + kAhead < 16) kop[i + kAhead] = read_k(kb, i + kAhead);
       if (i < kNJ) tile_load(s_b, kbase, rsrc_k, koff, kn, i);
       else if (i < 2 * kNJ) tile_load(s_a, vbase, rsrc_v, voff, vn, i - kNJ);
       s_step(sc[N], kop[i], i);
-      if (i + 2 < 16) {
-        xs[i + 2][0] = arg(i + 2, 0);
-        xs[i + 2][1] = arg(i + 2, 1);
-      }
       if (i + 1 < 16) {
-        ex[i + 1][0] = exp2f_fast(xs[i + 1][0]);
-        ex[i + 1][1] = exp2f_fast(xs[i + 1][1]);
+        ex[i + 1][0] = exp2f_fast(xpair(sc[B], i + 1, 0));
+        ex[i + 1][1] = exp2f_fast(xpair(sc[B], i + 1, 1));
       }
       ls[i & 1] += ex[i][0] + ex[i][1];
       pop[i >> 2][2 * (i & 3)] = (__bf16)ex[i][0];
@@ -326,24 +335,30 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
       __builtin_amdgcn_sched_barrier(0);
     }
     __builtin_amdgcn_sched_barrier(0);
-    // phase 2: PV MFMAs; sum of P(t) and row max of S(t+1) between them
+    // phase 2: PV MFMAs; S(t+1) turned into x values (pair i in step i) and
+    // their row max (pair i-1 in step i) between them
 #pragma unroll
     for (int i = 0; i < kAhead; ++i) vop[i] = read_v(vb, i);
-    // two accumulation chains for the row max
-    float mx[2] = {-INFINITY, -INFINITY};
+    float mx[2] = {-INFINITY, -INFINITY};   // two accumulation chains
+    auto xmax = [&](int j) __attribute__((always_inline)) {
+      mx[j & 1] = vmax(mx[j & 1], vmax(sc[N][j & 1][2 * (j >> 1)], sc[N][j & 1][2 * (j >> 1) + 1]));
+    };
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       if (i + kAhead < 16) vop[i + kAhead] = read_v(vb, i + kAhead);
       pv_step(vop[i], i);
-      mx[i & 1] = vmax(mx[i & 1], vmax(sc[N][i & 1][2 * (i >> 1)], sc[N][i & 1][2 * (i >> 1) + 1]));
+      sc[N][i & 1][2 * (i >> 1)] = __builtin_fmaf(sc[N][i & 1][2 * (i >> 1)], a.c, -msub);
+      sc[N][i & 1][2 * (i >> 1) + 1] = __builtin_fmaf(sc[N][i & 1][2 * (i >> 1) + 1], a.c, -msub);
+      if (i > 0) xmax(i - 1);
       if (i + kAhead < 16) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
     __builtin_amdgcn_sched_barrier(0);
+    xmax(15);
     l += ls[0] + ls[1];
-    rescale_test(vmax(mx[0], mx[1]));
+    rescale_test(vmax(mx[0], mx[1]), sc[N]);
   };
 
   lds_u8* const K0 = (lds_u8*)k_lds0;
@@ -377,8 +392,9 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   if (wave_active) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) s_step(sc[0], read_k(K0, i), i);
+    to_x(sc[0]);
     if ((t0 + 1) * kKT > w_full) mask_tile(t0, sc[0]);
-    rescale_test(row_max(sc[0]));
+    rescale_test(row_max(sc[0]), sc[0]);
   }
 
   // ---- step t reads K(t+1) and V(t) and loads K(t+2), V(t+1).  K(t) and
