@@ -54,7 +54,7 @@ def source_digest() -> str:
     version of the kernel are not reported."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("attn_kernel.h", "common.h"):
+    for f in ("attn_kernel.h", "attn_pipe.h", "common.h"):
         with open(os.path.join(ROOT, "paper_2607_00151_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -225,7 +225,7 @@ def main():
         "append": {"ms": app_ms, "bytes": app_bytes, "gbs": app_bytes / (app_ms * 1e-3) / 1e9},
         "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": attn_tflops / PEAK_BF16_TFLOPS,
-                     "traffic": stored_traffic("attn_kernel", attn_bytes)},
+                     "traffic": stored_traffic("attn_pipe_kernel", attn_bytes)},
         "paper_context": "paper reports up to 11.9x transform-point TTFT reduction end to end on "
                          "H100 80GB (SGLang, Qwen3-8B); no kernel-level numbers",
     }
