@@ -156,14 +156,14 @@ sa_status check_ctx(sa_ctx* ctx) {
   return SA_OK;
 }
 
-// Attention kernel variants: 32 * qt query rows per wave, `waves` waves per
-// work item; `pipe` selects the software-pipelined kernel.  SA_ATTN_VARIANT
-// overrides the default (tuning only).
+// Attention kernel variants: 0 = the software-pipelined kernel (default),
+// 1 = the phase-separated kernel (32 rows per wave, 4 waves).  The
+// SA_ATTN_VARIANT environment variable selects one (comparison and tuning).
 struct AttnVariant {
   int qt, waves, pipe;
 };
-constexpr AttnVariant kVariants[] = {{1, 4, 0}, {2, 2, 0}, {2, 4, 0}, {1, 4, 1}};
-constexpr int kDefaultVariant = 3;
+constexpr AttnVariant kVariants[] = {{1, 4, 1}, {1, 4, 0}};
+constexpr int kDefaultVariant = 0;
 
 AttnVariant attn_variant() {
   static int v = [] {
@@ -180,12 +180,8 @@ void launch_attn_p(AttnVariant v, bool pool_rsrc, dim3 grid, hipStream_t st, con
     hipLaunchKernelGGL((sa::attn_pipe_kernel<P, true>), grid, dim3(256), 0, st, a);
   else if (v.pipe)
     hipLaunchKernelGGL((sa::attn_pipe_kernel<P, false>), grid, dim3(256), 0, st, a);
-  else if (v.qt == 1 && v.waves == 4)
-    hipLaunchKernelGGL((sa::attn_kernel<P, 1, 4>), grid, dim3(256), 0, st, a);
-  else if (v.qt == 2 && v.waves == 2)
-    hipLaunchKernelGGL((sa::attn_kernel<P, 2, 2>), grid, dim3(128), 0, st, a);
   else
-    hipLaunchKernelGGL((sa::attn_kernel<P, 2, 4>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((sa::attn_kernel<P, 1, 4>), grid, dim3(256), 0, st, a);
 }
 
 // pool_rsrc: a layer's K (and V) pool spans < 2^31 bytes, so one buffer
