@@ -10,12 +10,19 @@
 //             P(t) = exp2(x(t))       VALU (32 exp, 16 cvt, 32 add per lane;
 //                                       the adds form l)
 //   phase 2:  O^T += V(t)^T P(t)^T    16 MFMAs
-//             x(t+1) = c S(t+1) - m   VALU (32 fma), its row max and the
-//                                       lazy rescale test
+//             row max of x(t+1)       VALU (16 max3) and the lazy rescale test
 // with K one tile ahead of V.  The VALU work of each phase depends only on
 // results of the previous phase, so it issues between the MFMAs.  Steps whose
 // next tile needs the causal mask, and the last step, run the same sequence
 // without the interleaving.
+//
+// The exponent x = c s - m (c = softmax scale times log2 e, m the offset in
+// use) comes out of the MFMA itself: the query rows are scaled by c once, when
+// they are loaded, and every S accumulation starts from -m instead of zero.
+// That takes the 32 fma per lane and tile off the VALU.  The price is one
+// more bf16 rounding, of c q: each x moves by at most 2^-9 sum_d |c q_d k_d|,
+// so the log-sum-exp moves by at most ln 2 times that, over the row's keys;
+// the output's own error stays far inside its tolerance.
 #pragma once
 
 #include "attn_kernel.h"
@@ -28,24 +35,56 @@ struct IntC {
   static constexpr int value = N;
 };
 
+constexpr int kPipeWaves = 4;                              // waves per group, 32 rows each
+constexpr int kPipeRows = 32 * kPipeWaves;                 // query rows per work item
+constexpr int kTileBytes = kKT * kHD * 2;                  // one K or V tile, 16 KB
+
+// LDS of one group: its double-buffered K and V tiles.  A second group also
+// names the first group's partial-result area (four 16 KB arrays and a 2 KB
+// array of row statistics), which the other group fills at the end.
+struct PipeLds {
+  lds_u8 *k0, *k1, *v0, *v1;
+  lds_u8 *x0, *x1, *x2, *x3;
+  __attribute__((address_space(3))) float* ml;
+};
+
+// Page slots of an item are checked once: true if every page its keys need is
+// present and in range.  Every thread of the block takes part (one barrier).
+template <int P>
+__device__ __forceinline__ bool item_table_ok(const AttnArgs& a, const AttnItem& it, int nthreads) {
+  constexpr int kPagesPerTile = kKT / P;
+  const int32_t pt_base = ld_uniform(a.indptr + it.seq);
+  const int32_t pt_count = ld_uniform(a.indptr + it.seq + 1) - pt_base;
+  const int t0 = it.kv_begin / kKT;
+  const int t1 = (it.kv_end + kKT - 1) / kKT;
+  bool bad = pt_count < (it.kv_end + P - 1) / P;
+  for (int pg = t0 * kPagesPerTile + (int)threadIdx.x; pg < min(t1 * kPagesPerTile, pt_count); pg += nthreads) {
+    const int32_t s = a.indices[pt_base + pg];
+    bad |= !(s >= 0 && s < a.num_slots);
+  }
+  return !__syncthreads_or(bad);
+}
+
+// One group of four waves runs the item's rows over the keys
+// [g_lo, g_hi): the whole item when kGroups == 1; with two groups, group 0
+// takes the first half of the item's key tiles and group 1 the rest, and the
+// two meet at the end to merge their partial results.  With two groups every
+// step holds two barriers (one before each phase) and group 1 runs one
+// barrier behind group 0, so on each SIMD one group's phase 1 overlaps the
+// other's phase 2.
+//
 // kPoolRsrc: a layer's K (and V) pool spans < 2^31 bytes, so one buffer
 // resource per pool reaches every page through the 32-bit scalar offset;
 // otherwise each page load builds a resource for its page.
-template <int P, bool kPoolRsrc>
-__global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
+template <int P, bool kPoolRsrc, int kGroups, int GRP>
+__device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs& a, const AttnItem& it,
+                                                                 const SeqDesc& sd, const PipeLds& L) {
   static_assert(P == 16 || P == 32, "page size");
-  constexpr int WAVES = 4;
-  constexpr int kRows = 32 * WAVES;                        // rows per item
-  constexpr int kTileBytes = kKT * kHD * 2;                // 16 KB
+  constexpr int WAVES = kPipeWaves;
+  constexpr int kRows = kPipeRows;
   constexpr int kPagesPerTile = kKT / P;
   constexpr int kNJ = 16 / WAVES;                          // loads per wave per tile and operand
   constexpr int kAhead = 2;                                // operand reads issued this many steps ahead
-  __shared__ __attribute__((aligned(1024))) uint8_t k_lds0[kTileBytes], k_lds1[kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t v_lds0[kTileBytes], v_lds1[kTileBytes];
-
-  const AttnItem it = ld_uniform(a.items + blockIdx.x);
-  if (it.kv_begin >= it.kv_end) return;                     // padding item
-  const SeqDesc sd = ld_uniform(a.seqs + it.seq);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -62,15 +101,28 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   const int head = it.kvh * G + (rr - tok * G);
   const int qpos = pre + tok;
 
+  // this group's keys [g_lo, g_hi) and tiles [t0, t1)
+  const int ti0 = it.kv_begin / kKT;
+  const int ti1 = (it.kv_end + kKT - 1) / kKT;
+  const int tmid = ti0 + (ti1 - ti0 + 1) / 2;
+  const int g_lo = (kGroups == 2 && GRP == 1) ? tmid * kKT : it.kv_begin;
+  const int g_hi = (kGroups == 2 && GRP == 0) ? min(it.kv_end, tmid * kKT) : it.kv_end;
+  const int t0 = g_lo / kKT;
+  const int t1 = g_lo < g_hi ? (g_hi + kKT - 1) / kKT : t0;
+
   const int wrow0 = it.row0 + wave * 32;
   const bool wave_active = wrow0 < rows_total;
-  const int w_full = min(it.kv_end, pre + wrow0 / G + 1);    // keys below are visible to all rows
+  const int w_full = min(g_hi, pre + wrow0 / G + 1);         // keys below are visible to all rows
 
-  bf16x8 qop[8];
+  bf16x8 qop[8];             // c q, rounded to bf16
   {
     const uint16_t* qrow = a.q + ((int64_t)(sd.q_start + tok) * a.Hq + head) * kHD;
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) qop[ks] = ld_bf16x8(qrow + (2 * ks + hh) * 8);
+    for (int ks = 0; ks < 8; ++ks) {
+      const bf16x8 raw = ld_bf16x8(qrow + (2 * ks + hh) * 8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qop[ks][e] = (__bf16)((float)raw[e] * a.c);
+    }
   }
 
   const int32_t pt_base = ld_uniform(a.indptr + it.seq);
@@ -101,17 +153,11 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   };
   auto slot_ok = [&](int32_t s) __attribute__((always_inline)) { return s >= 0 && s < a.num_slots; };
 
-  const int t0 = it.kv_begin / kKT;
-  const int t1 = (it.kv_end + kKT - 1) / kKT;
-
-  // The item's page slots are checked once: a block whose table is intact
-  // (every page its keys need present and in range) loads tiles without
-  // per-page tests; otherwise every tile takes the checked path, which
-  // zero-fills what it cannot load and raises the error flag.
-  bool table_bad = pt_count < (it.kv_end + P - 1) / P;
-  for (int pg = t0 * kPagesPerTile + tid; pg < min(t1 * kPagesPerTile, pt_count); pg += kRows * 2)
-    table_bad |= !slot_ok(a.indices[pt_base + pg]);
-  const bool table_ok = !__syncthreads_or(table_bad);
+  // A block whose table is intact (table_ok) loads tiles without per-page
+  // tests; otherwise every tile takes the checked path, which zero-fills
+  // what it cannot load and raises the error flag.  The check itself runs
+  // while the first tiles load, which take the checked path.
+  bool table_ok = false;
   const uint32_t pool_bytes = kPoolRsrc ? (uint32_t)(a.num_slots * slot_bytes) : 0u;
   const __amdgpu_buffer_rsrc_t rsrc_k =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.k), (short)0, (int)pool_bytes, 0x00020000);
@@ -122,7 +168,7 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   auto load_op = [&](int t, const Slots& S, const char* base, const __amdgpu_buffer_rsrc_t& rsrc, const int* off,
                      lds_u8* dst) __attribute__((always_inline)) {
     const int ts = t * kKT;
-    if (table_ok && ts + kKT <= it.kv_end) {
+    if (table_ok && ts + kKT <= g_hi) {
 #pragma unroll
       for (int j = 0; j < kNJ; ++j) {
         const int gb = j * WAVES + wave;
@@ -139,9 +185,9 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
       for (int j = 0; j < kNJ; ++j) {
         const int gb = j * WAVES + wave;
         const int32_t s = S.s[(4 * gb) / P];
-        const bool page_needed = ts + 4 * gb < it.kv_end;
+        const bool page_needed = ts + 4 * gb < g_hi;
         bad |= page_needed && !slot_ok(s);
-        const bool ld = page_needed && slot_ok(s) && ts + 4 * gb + (lane >> 4) < it.kv_end;
+        const bool ld = page_needed && slot_ok(s) && ts + 4 * gb + (lane >> 4) < g_hi;
         if (ld) {
           lds_dma16(base + (int64_t)s * slot_bytes, (uint32_t)slot_bytes, off[j],
                     (__attribute__((address_space(3))) void*)(dst + gb * 1024));
@@ -161,6 +207,7 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   float m_used = -INFINITY;  // exponent offset in use (log2 domain)
   float msub = 0.f;          // m_used, or 0 while it is -inf
   float l = 0.f;             // this lane's share of the denominator
+  f32x16 negm = f32x16{};    // -msub in every element: where each S accumulation starts
   f32x16 sc[2][2];           // [buffer][32-key block] scores of tiles t and t + 1
   bf16x8 pop[4];             // [16-key group] probabilities of tile t
 
@@ -190,18 +237,10 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
     return vop;
   };
   auto s_step = [&](f32x16* S, bf16x8 kop, int i) __attribute__((always_inline)) {
-    S[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[i >> 1], i < 2 ? f32x16{} : S[i & 1], 0, 0, 0);
+    S[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[i >> 1], i < 2 ? negm : S[i & 1], 0, 0, 0);
   };
   auto pv_step = [&](bf16x8 vop, int i) __attribute__((always_inline)) {
     oacc[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[i >> 2], oacc[i & 3], 0, 0, 0);
-  };
-  // A tile's scores are rewritten in place as x = c s - msub, the exponent of
-  // their probability against the offset in use.
-  auto to_x = [&](f32x16* S) __attribute__((always_inline)) {
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) S[kt][e] = __builtin_fmaf(S[kt][e], a.c, -msub);
   };
   // probabilities of pair j (elements 2j, 2j + 1 of the tile, in P^T slot
   // order: group j >> 2, slots 2 (j & 3) and 2 (j & 3) + 1)
@@ -219,7 +258,7 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   };
   auto mask_tile = [&](int t, f32x16* S) __attribute__((always_inline)) {
     const int ts = t * kKT;
-    const int lim = min(qpos, it.kv_end - 1);
+    const int lim = min(qpos, g_hi - 1);
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
@@ -241,6 +280,8 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
       const float msub_new = (m_used == -INFINITY) ? 0.f : m_used;
       const float shift = msub_new - msub;
       msub = msub_new;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) negm[e] = -msub;
       l *= alpha;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
@@ -266,22 +307,26 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   // moves to sc[0]
   auto plain_step = [&](int t, const lds_u8* kb, const lds_u8* vb) __attribute__((always_inline)) {
     const bool has_next = t + 1 < t1;
-    if (has_next) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) s_step(sc[1], read_k(kb, i), i);
-    }
     float ls = 0.f;
+    if (wave_active) {
+      if (has_next) {
 #pragma unroll
-    for (int j = 0; j < 16; ++j) ls += exp_pair(sc[0], j);
+        for (int i = 0; i < 16; ++i) s_step(sc[1], read_k(kb, i), i);
+      }
 #pragma unroll
-    for (int i = 0; i < 16; ++i) pv_step(read_v(vb, i), i);
-    l += ls;
-    if (has_next) {
-      to_x(sc[1]);
-      if ((t + 2) * kKT > w_full) mask_tile(t + 1, sc[1]);
-      rescale_test(row_max(sc[1]), sc[1]);
-      sc[0][0] = sc[1][0];
-      sc[0][1] = sc[1][1];
+      for (int j = 0; j < 16; ++j) ls += exp_pair(sc[0], j);
+    }
+    if constexpr (kGroups == 2) lds_barrier();
+    if (wave_active) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) pv_step(read_v(vb, i), i);
+      l += ls;
+      if (has_next) {
+        if ((t + 2) * kKT > w_full) mask_tile(t + 1, sc[1]);
+        rescale_test(row_max(sc[1]), sc[1]);
+        sc[0][0] = sc[1][0];
+        sc[0][1] = sc[1][1];
+      }
     }
   };
 
@@ -335,39 +380,33 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
       __builtin_amdgcn_sched_barrier(0);
     }
     __builtin_amdgcn_sched_barrier(0);
-    // phase 2: PV MFMAs; S(t+1) turned into x values (pair i in step i) and
-    // their row max (pair i-1 in step i) between them
+    if constexpr (kGroups == 2) lds_barrier();
+    // phase 2: PV MFMAs; the row max of x(t+1) (pair i in step i) between them
 #pragma unroll
     for (int i = 0; i < kAhead; ++i) vop[i] = read_v(vb, i);
     float mx[2] = {-INFINITY, -INFINITY};   // two accumulation chains
-    auto xmax = [&](int j) __attribute__((always_inline)) {
-      mx[j & 1] = vmax(mx[j & 1], vmax(sc[N][j & 1][2 * (j >> 1)], sc[N][j & 1][2 * (j >> 1) + 1]));
-    };
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       if (i + kAhead < 16) vop[i + kAhead] = read_v(vb, i + kAhead);
       pv_step(vop[i], i);
-      sc[N][i & 1][2 * (i >> 1)] = __builtin_fmaf(sc[N][i & 1][2 * (i >> 1)], a.c, -msub);
-      sc[N][i & 1][2 * (i >> 1) + 1] = __builtin_fmaf(sc[N][i & 1][2 * (i >> 1) + 1], a.c, -msub);
-      if (i > 0) xmax(i - 1);
+      mx[i & 1] = vmax(mx[i & 1], vmax(sc[N][i & 1][2 * (i >> 1)], sc[N][i & 1][2 * (i >> 1) + 1]));
       if (i + kAhead < 16) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
     __builtin_amdgcn_sched_barrier(0);
-    xmax(15);
     l += ls[0] + ls[1];
     rescale_test(vmax(mx[0], mx[1]), sc[N]);
   };
 
-  lds_u8* const K0 = (lds_u8*)k_lds0;
-  lds_u8* const K1 = (lds_u8*)k_lds1;
-  lds_u8* const V0 = (lds_u8*)v_lds0;
-  lds_u8* const V1 = (lds_u8*)v_lds1;
+  lds_u8* const K0 = L.k0;
+  lds_u8* const K1 = L.k1;
+  lds_u8* const V0 = L.v0;
+  lds_u8* const V1 = L.v1;
 
   // ---- prologue: K(t0), V(t0), K(t0 + 1); S(t0) and its rescale test
-  {
+  if (t0 < t1) {
     const Slots s0 = fetch(t0);
     load_op(t0, s0, kbase, rsrc_k, koff, K0);
     load_op(t0, s0, vbase, rsrc_v, voff, V0);
@@ -387,12 +426,13 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
       return __builtin_bit_cast(slot_vec, __builtin_amdgcn_raw_buffer_load_b64(rsrc_pt, t * 8, 0, 0));
   };
   slot_vec v_next = fetch_vec(t0 + 2);                      // pages of tile t + 2, in flight
+  table_ok = item_table_ok<P>(a, it, 64 * WAVES * kGroups);
   __builtin_amdgcn_s_waitcnt(0x0070);
   lds_barrier();
-  if (wave_active) {
+  if (kGroups == 2 && GRP == 1) lds_barrier();             // group 1 runs a barrier behind
+  if (wave_active && t0 < t1) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) s_step(sc[0], read_k(K0, i), i);
-    to_x(sc[0]);
     if ((t0 + 1) * kKT > w_full) mask_tile(t0, sc[0]);
     rescale_test(row_max(sc[0]), sc[0]);
   }
@@ -452,8 +492,55 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   for (; t < t1; ++t) {
     const bool odd = (t - t0) & 1;
     top(t, odd ? K1 : K0, odd ? V0 : V1);
-    if (wave_active) plain_step(t, odd ? K0 : K1, odd ? V1 : V0);
+    plain_step(t, odd ? K0 : K1, odd ? V1 : V0);
     advance(t);
+  }
+
+  if constexpr (kGroups == 2) {
+    // Both groups pass the same number of barriers: group g has passed
+    // 1 + g + 2 (its steps) so far; pad to the larger count, then one more
+    // barrier frees the tile buffers for group 1's partial results and
+    // another publishes them.
+    const int n0 = tmid - ti0, n1 = ti1 - tmid;              // steps of each group
+    const int passed = 1 + GRP + 2 * (GRP == 0 ? n0 : n1);
+    const int total = max(1 + 2 * n0, 2 + 2 * n1);
+    for (int k = passed; k < total; ++k) lds_barrier();
+    __builtin_amdgcn_s_waitcnt(0x0070);                     // no tile load of mine in flight
+    lds_barrier();
+    auto slot = [&](int k) __attribute__((always_inline)) {
+      lds_u8* const x[4] = {L.x0, L.x1, L.x2, L.x3};
+      return (__attribute__((address_space(3))) f32x4*)(x[k >> 2] + ((k & 3) * WAVES + wave) * 1024 + lane * 16);
+    };
+    if (GRP == 1) {
+      if (wave_active) {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const int dt = k >> 2, i = k & 3;
+          *slot(k) = f32x4{oacc[dt][4 * i], oacc[dt][4 * i + 1], oacc[dt][4 * i + 2], oacc[dt][4 * i + 3]};
+        }
+        L.ml[wave * 64 + lane] = m_used;
+        L.ml[kRows * 2 + wave * 64 + lane] = l;
+      }
+      lds_barrier();
+      return;
+    }
+    lds_barrier();
+    if (!wave_active) return;
+    // merge: both partials are sums against their own exponent offsets
+    const float m_b = L.ml[wave * 64 + lane];
+    const float l_b = L.ml[kRows * 2 + wave * 64 + lane];
+    const float m_new = fmaxf(m_used, m_b);
+    const float alpha = (m_used == -INFINITY) ? 0.f : exp2f_fast(m_used - m_new);
+    const float beta = (m_b == -INFINITY) ? 0.f : exp2f_fast(m_b - m_new);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int dt = k >> 2, i = k & 3;
+      const f32x4 ob = *slot(k);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) oacc[dt][4 * i + e] = oacc[dt][4 * i + e] * alpha + ob[e] * beta;
+    }
+    l = l * alpha + l_b * beta;
+    m_used = m_new;
   }
 
   if (!wave_active) return;
@@ -487,6 +574,45 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
         *(f32x4*)(po + d) = w;
       }
     if (hh == 0) a.part_lse[(int64_t)it.part * kRows + lrow] = lse2;
+  }
+}
+
+// One group of four waves per block, two blocks per CU.
+template <int P, bool kPoolRsrc>
+__global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(1024))) uint8_t k_lds0[kTileBytes], k_lds1[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t v_lds0[kTileBytes], v_lds1[kTileBytes];
+  const AttnItem it = ld_uniform(a.items + blockIdx.x);
+  if (it.kv_begin >= it.kv_end) return;                     // padding item
+  const SeqDesc sd = ld_uniform(a.seqs + it.seq);
+  const PipeLds L{(lds_u8*)k_lds0, (lds_u8*)k_lds1, (lds_u8*)v_lds0, (lds_u8*)v_lds1,
+                  nullptr, nullptr, nullptr, nullptr, nullptr};
+  pipe_group<P, kPoolRsrc, 1, 0>(a, it, sd, L);
+}
+
+// Two groups of four waves per block on the same rows, each over half of the
+// item's key tiles, one block per CU; the halves merge in LDS.
+template <int P, bool kPoolRsrc>
+__global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(1024))) uint8_t k_a0[kTileBytes], k_a1[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t v_a0[kTileBytes], v_a1[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t k_b0[kTileBytes], k_b1[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t v_b0[kTileBytes], v_b1[kTileBytes];
+  __shared__ float ml[4 * kPipeRows];
+  const AttnItem it = ld_uniform(a.items + blockIdx.x);
+  if (it.kv_begin >= it.kv_end) return;                     // padding item
+  const SeqDesc sd = ld_uniform(a.seqs + it.seq);
+  lds_u8* const xb0 = (lds_u8*)k_b0;
+  lds_u8* const xb1 = (lds_u8*)k_b1;
+  lds_u8* const xb2 = (lds_u8*)v_b0;
+  lds_u8* const xb3 = (lds_u8*)v_b1;
+  __attribute__((address_space(3))) float* const mlp = (__attribute__((address_space(3))) float*)ml;
+  if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) < kPipeWaves) {
+    const PipeLds L{(lds_u8*)k_a0, (lds_u8*)k_a1, (lds_u8*)v_a0, (lds_u8*)v_a1, xb0, xb1, xb2, xb3, mlp};
+    pipe_group<P, kPoolRsrc, 2, 0>(a, it, sd, L);
+  } else {
+    const PipeLds L{xb0, xb1, xb2, xb3, xb0, xb1, xb2, xb3, mlp};
+    pipe_group<P, kPoolRsrc, 2, 1>(a, it, sd, L);
   }
 }
 

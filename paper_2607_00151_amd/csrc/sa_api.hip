@@ -157,12 +157,14 @@ sa_status check_ctx(sa_ctx* ctx) {
 }
 
 // Attention kernel variants: 0 = the software-pipelined kernel (default),
-// 1 = the phase-separated kernel (32 rows per wave, 4 waves).  The
-// SA_ATTN_VARIANT environment variable selects one (comparison and tuning).
+// 1 = the phase-separated kernel (32 rows per wave, 4 waves), 2 = the
+// pipelined kernel with two groups of four waves per block splitting each
+// item's keys.  The SA_ATTN_VARIANT environment variable selects one
+// (comparison and tuning).
 struct AttnVariant {
   int qt, waves, pipe;
 };
-constexpr AttnVariant kVariants[] = {{1, 4, 1}, {1, 4, 0}};
+constexpr AttnVariant kVariants[] = {{1, 4, 1}, {1, 4, 0}, {1, 4, 2}};
 constexpr int kDefaultVariant = 0;
 
 AttnVariant attn_variant() {
@@ -176,7 +178,11 @@ AttnVariant attn_variant() {
 
 template <int P>
 void launch_attn_p(AttnVariant v, bool pool_rsrc, dim3 grid, hipStream_t st, const sa::AttnArgs& a) {
-  if (v.pipe && pool_rsrc)
+  if (v.pipe == 2 && pool_rsrc)
+    hipLaunchKernelGGL((sa::attn_pp_kernel<P, true>), grid, dim3(512), 0, st, a);
+  else if (v.pipe == 2)
+    hipLaunchKernelGGL((sa::attn_pp_kernel<P, false>), grid, dim3(512), 0, st, a);
+  else if (v.pipe && pool_rsrc)
     hipLaunchKernelGGL((sa::attn_pipe_kernel<P, true>), grid, dim3(256), 0, st, a);
   else if (v.pipe)
     hipLaunchKernelGGL((sa::attn_pipe_kernel<P, false>), grid, dim3(256), 0, st, a);
@@ -523,8 +529,12 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
   // Two blocks share a CU, and with a grid of at most two rounds the
   // dispatcher pairs block i with block i + (number of CUs) (measured): the
   // second round is reversed so the longest items share CUs with the
-  // shortest and every CU gets about the same work.
-  auto pair_rounds = [](std::vector<sa::AttnItem>& q, size_t first_round) {
+  // shortest and every CU gets about the same work.  A kernel with one block
+  // per CU keeps the longest-first order: each later block goes to the CU
+  // that frees first.
+  const bool one_block_per_cu = var.pipe == 2;
+  auto pair_rounds = [one_block_per_cu](std::vector<sa::AttnItem>& q, size_t first_round) {
+    if (one_block_per_cu) return;
     if (q.size() > first_round && q.size() <= 2 * first_round) std::reverse(q.begin() + first_round, q.end());
   };
   std::vector<sa::AttnItem> items;

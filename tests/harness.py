@@ -136,6 +136,34 @@ def sample_rows(w: Workload, per_seq: int, seed: int = 0):
     return np.asarray(toks, dtype=np.int64), np.asarray(heads, dtype=np.int32)
 
 
+def lse_tolerance(w: Workload, toks: np.ndarray, heads: np.ndarray, slack: float = 1e-4) -> np.ndarray:
+    """Per-row bound on the device LSE error (natural log).
+
+    The kernel rounds c q (c = scale log2 e) to bf16 once, so each exponent
+    x_j = c q.k_j moves by at most 2^-9 sum_d |c q_d k_jd|; the log-sum-exp of
+    the row moves by no more than the largest such shift over its visible
+    keys (it is monotone and commutes with a common shift), times ln 2 to go
+    back from base 2.  slack covers the fp32 arithmetic of the rest.
+    """
+    c = w.scale * np.log2(np.e)
+    G = w.num_q_heads // w.num_kv_heads
+    qf = np.abs(bf16_to_f64(w.q[toks, heads]))               # [n][D]
+    kf = w.k
+    bound = np.zeros(len(toks))
+    seq = np.searchsorted(w.q_indptr, toks, side="right") - 1
+    for b in np.unique(seq):
+        kv0 = int(w.kv_indptr[b])
+        pre = int(w.kv[b]) - int(w.qlen[b])
+        for g in np.unique(heads[seq == b] // G):
+            sel = np.nonzero((seq == b) & (heads // G == g))[0]
+            pos = pre + (toks[sel] - int(w.q_indptr[b]))       # last visible key of each row
+            kb = np.abs(bf16_to_f64(kf[kv0: kv0 + int(pos.max()) + 1, g]))   # [keys][D]
+            s = (qf[sel] * abs(c)) @ kb.T                      # sum_d |c q_d k_jd|
+            s[np.arange(kb.shape[0])[None, :] > pos[:, None]] = 0.0
+            bound[sel] = s.max(axis=1)
+    return np.log(2.0) * 2.0 ** -9 * bound + slack
+
+
 def compare(got_bits: np.ndarray, ref: np.ndarray, max_tol=2e-2, mean_tol=2e-3):
     """bf16 device output vs float64 oracle: returns (max_abs, mean_abs)."""
     got = bf16_to_f64(got_bits)

@@ -1,10 +1,11 @@
-"""GPU parity of the alternative attention kernel.
+"""GPU parity of the alternative attention kernels.
 
 The library picks its attention kernel once per process (the
-SA_ATTN_VARIANT environment variable; variant 1 is the phase-separated
-kernel, variant 0 the software-pipelined default the other GPU tests use).
-This test runs the small attention parity cases and a split/merge case in a
-child process with variant 1, against the same oracle and tolerances.
+SA_ATTN_VARIANT environment variable; variant 0 is the software-pipelined
+default the other GPU tests use, 1 the phase-separated kernel, 2 the
+pipelined kernel with two key-splitting groups per block).  This test runs
+the small attention parity cases and a split/merge case in a child process
+per variant, against the same oracle and tolerances.
 """
 import os
 import subprocess
@@ -24,12 +25,12 @@ import oracle, workloads
 import paper_2607_00151_amd as sa
 from workloads.configs import build
 from harness import attention, build_cache, compare, dev_u16, host_u16, layout_of
-from test_gpu_parity import small, SMALL, MAX_TOL, MEAN_TOL, LSE_TOL
+from test_gpu_parity import small, SMALL, MAX_TOL, MEAN_TOL, check_lse
 ctx = sa.Context(0)
 cases = [(n, small(n)) for n in SMALL]
 cases.append(("split", build("split", 21, 8, 1, 128, 16, [5000, 3000, 70, 0], [1, 1, 3, 1])))
 for name, w in cases:
-    print("variant-1 attention", name, flush=True)
+    print("variant {variant} attention", name, flush=True)
     L = layout_of(w)
     kp, vp, ip, ix = build_cache(w)
     o, lse = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
@@ -37,7 +38,7 @@ for name, w in cases:
     ref, ref_lse, _ = oracle.attention_all(w.q, w.k, w.v, w.q_indptr, w.kv_indptr,
                                            w.num_q_heads, w.num_kv_heads, w.scale)
     mx, mean = compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
-    assert np.abs(lse.cpu().numpy() - ref_lse).max() <= LSE_TOL
+    check_lse(w, lse.cpu().numpy(), ref_lse)
     print("  ok max %.3e mean %.3e" % (mx, mean), flush=True)
 ctx.close()
 print("ALL-OK", flush=True)
@@ -45,9 +46,10 @@ print("ALL-OK", flush=True)
 
 
 @pytest.mark.timeout(300)
-def test_phase_separated_kernel_parity():
-    code = CHILD.format(root=ROOT, tests=os.path.join(ROOT, "tests"))
-    env = dict(os.environ, SA_ATTN_VARIANT="1")
+@pytest.mark.parametrize("variant", [1, 2])
+def test_variant_kernel_parity(variant):
+    code = CHILD.format(root=ROOT, tests=os.path.join(ROOT, "tests"), variant=variant)
+    env = dict(os.environ, SA_ATTN_VARIANT=str(variant))
     r = subprocess.run([sys.executable, "-u", "-c", code], env=env, cwd=ROOT,
                        capture_output=True, text=True, timeout=280)
     print(r.stdout[-4000:])
