@@ -49,6 +49,7 @@ struct AttnItem {
   int32_t kv_begin;  // first key, multiple of kKT
   int32_t kv_end;    // one past the last key this item reads (<= kv_len)
   int32_t part;      // -1: final output; else index of this item's partial slot
+  int32_t boost;     // steps at the start that run at raised wave priority (0: none)
 };
 
 struct SeqDesc {

@@ -443,6 +443,12 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
     __builtin_amdgcn_s_waitcnt(0x0070);                     // my loads of K(t+1), V(t) landed
     lds_barrier();                                          // everyone's; the next buffers are free
   };
+  // the item's first `boost` steps run at raised wave priority
+  const int t_boost = t0 + (kGroups == 1 ? it.boost : 0);
+  auto priority = [&](int t) __attribute__((always_inline)) {
+    if (t == t_boost) __builtin_amdgcn_s_setprio(0);
+  };
+  if (t_boost > t0) __builtin_amdgcn_s_setprio(1);
   auto top = [&](int t, lds_u8* kn, lds_u8* vn) __attribute__((always_inline)) {
     wait_tiles();
     if (t + 2 < t1) load_op(t + 2, s_b, kbase, rsrc_k, koff, kn);
@@ -469,14 +475,17 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
                          : t0;
   int t = t0;
   for (; t + 1 < t_fast; t += 2) {
+    priority(t);
     wait_tiles();
     advance_fast(t);
     fast_step(IntC<0>{}, K1, V0, K0, V1);
+    priority(t + 1);
     wait_tiles();
     advance_fast(t + 1);
     fast_step(IntC<1>{}, K0, V1, K1, V0);
   }
   if (t < t_fast) {
+    priority(t);
     wait_tiles();
     advance_fast(t);
     fast_step(IntC<0>{}, K1, V0, K0, V1);
@@ -491,6 +500,7 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
   }
   for (; t < t1; ++t) {
     const bool odd = (t - t0) & 1;
+    priority(t);
     top(t, odd ? K1 : K0, odd ? V0 : V1);
     plain_step(t, odd ? K0 : K1, odd ? V1 : V0);
     advance(t);

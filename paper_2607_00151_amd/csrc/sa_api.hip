@@ -551,6 +551,25 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
     for (const Work& w : work) items.push_back(w.it);
     pair_rounds(items, (size_t)ctx->num_cu);
   }
+  // Finishing a CU's two blocks together.  Of two co-resident blocks the
+  // older (first-round) one wins the SIMD's issue arbitration: measured at
+  // c2, the favoured block advances at about 1.4 times the other's rate
+  // (kSlowShare = 0.715 of it), and a block left alone on the CU uses it
+  // less well than the pair.  The later block of a pair therefore runs its
+  // first `boost` steps at raised priority, chosen so that under those rates
+  // both blocks end at the same time: with S = L_old + L_new tiles and
+  // D = L_old - L_new, boost = (S / (1 + r) - D / (1 - r)) / 2.
+  if (!one_block_per_cu && items.size() > (size_t)ctx->num_cu && items.size() <= 2 * (size_t)ctx->num_cu) {
+    constexpr double kSlowShare = 0.715;
+    auto tiles_of = [](const sa::AttnItem& x) {
+      return x.kv_end > x.kv_begin ? (x.kv_end + sa::kKT - 1) / sa::kKT - x.kv_begin / sa::kKT : 0;
+    };
+    for (size_t b = ctx->num_cu; b < items.size(); ++b) {
+      const double l_new = tiles_of(items[b]), l_old = tiles_of(items[b - ctx->num_cu]);
+      const double x = 0.5 * ((l_old + l_new) / (1.0 + kSlowShare) - (l_old - l_new) / (1.0 - kSlowShare));
+      items[b].boost = (int32_t)std::lround(std::min(std::max(x, 0.0), l_new));
+    }
+  }
 
   if (n_parts > 0) {
     const size_t need = (size_t)n_parts * rows_item * (sa::kHD + 1) * sizeof(float);
