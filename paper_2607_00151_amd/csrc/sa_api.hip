@@ -351,7 +351,7 @@ sa_status sa_kv_assemble(sa_ctx* ctx, const sa_layout* layout, const void* k_src
   if (h_keep_indptr[batch] > 0 && !h_keep_spans) return fail(SA_ERR_NULL, "h_keep_spans is NULL");
   if (num_fresh < 0 || dst_capacity < 0) return fail(SA_ERR_SHAPE, "negative capacity");
   const int P = layout->page_size;
-  std::vector<sa::AsmSpan> spans;
+  std::vector<sa::AsmUnit> unit_list;
   std::vector<int32_t> dst_indptr(batch + 1, 0), dst_len(batch, 0);
   int64_t units = 0, n_dst = 0;
   for (int b = 0; b < batch; ++b) {
@@ -367,7 +367,8 @@ sa_status sa_kv_assemble(sa_ctx* ctx, const sa_layout* layout, const void* k_src
       if (beg < prev_end || beg >= end || end > n_src_pages)
         return fail(SA_ERR_RANGE, "sequence %d: keep span [%d, %d) invalid (previous end %d, %d pages)",
                     b, beg, end, prev_end, n_src_pages);
-      spans.push_back({b, beg, kept_pages, (int32_t)units});
+      for (int p = beg; p < end; ++p)
+        unit_list.push_back({b, p, (int32_t)(n_dst + kept_pages + (p - beg))});
       for (int p = beg; p < end; ++p) kept += std::min(P, h_src_len[b] - p * P);
       kept_pages += end - beg;
       units += end - beg;
@@ -394,7 +395,7 @@ sa_status sa_kv_assemble(sa_ctx* ctx, const sa_layout* layout, const void* k_src
   memcpy(h_dst_len, dst_len.data(), sizeof(int32_t) * batch);
 
   PlanImage img;
-  const size_t o_sp = img.add(spans.data(), spans.size());
+  const size_t o_un = img.add(unit_list.data(), unit_list.size());
   const size_t o_ip = img.add(dst_indptr.data(), dst_indptr.size());
   uint8_t* dev = nullptr;
   s = upload_plan(ctx, kPlanAssemble, img, (hipStream_t)stream, &dev);
@@ -405,7 +406,7 @@ sa_status sa_kv_assemble(sa_ctx* ctx, const sa_layout* layout, const void* k_src
   a.v_src = (const uint16_t*)v_src;
   a.k_dst = (uint16_t*)k_dst;
   a.v_dst = (uint16_t*)v_dst;
-  a.spans = (const sa::AsmSpan*)(dev + o_sp);
+  a.units = (const sa::AsmUnit*)(dev + o_un);
   a.dst_indptr = (const int32_t*)(dev + o_ip);
   a.src_indptr = src.indptr;
   a.src_indices = src.indices;
@@ -416,13 +417,12 @@ sa_status sa_kv_assemble(sa_ctx* ctx, const sa_layout* layout, const void* k_src
   a.num_slots = layout->num_slots;
   a.slot_elems = slot_elems(layout);
   a.layer_elems = layer_elems(layout);
-  a.n_spans = (int32_t)spans.size();
   a.n_units = (int32_t)units;
   a.n_dst = (int32_t)n_dst;
   a.B = batch;
-  const int64_t table_blocks = (std::max<int64_t>(n_dst, batch + 1) + 255) / 256;
+  const int64_t table_blocks = (std::max<int64_t>(n_dst, batch + 1) + sa::kAsmThreads - 1) / sa::kAsmThreads;
   const int64_t gx = std::max<int64_t>(units, table_blocks);
-  hipLaunchKernelGGL(sa::assemble_kernel, dim3((unsigned)gx, (unsigned)layout->num_layers), dim3(256),
+  hipLaunchKernelGGL(sa::assemble_kernel, dim3((unsigned)gx, (unsigned)layout->num_layers), dim3(sa::kAsmThreads),
                      0, (hipStream_t)stream, a);
   SA_HIP(hipGetLastError());
   return SA_OK;
