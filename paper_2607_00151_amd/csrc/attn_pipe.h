@@ -557,33 +557,41 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
   const float l_tot = pair_sum(l);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   const float lse2 = l_tot > 0.f ? m_used + __builtin_amdgcn_logf(l_tot) : -INFINITY;
+  // The output row is worked out again from the lane index here rather than
+  // kept from the start: values live across the loops beyond its registers
+  // are spilled to scratch memory.
+  const int lane_o = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+  const int hh_o = lane_o >> 5;
+  const int o_row = it.row0 + wave * 32 + (lane_o & 31);
+  const int o_tok = o_row / G;
+  const int o_head = it.kvh * G + (o_row - o_tok * G);
   if (it.part < 0) {
-    if (row_valid) {
-      uint16_t* orow = a.o + ((int64_t)(sd.q_start + tok) * a.Hq + head) * kHD;
+    if (o_row < rows_total) {
+      uint16_t* orow = a.o + ((int64_t)(sd.q_start + o_tok) * a.Hq + o_head) * kHD;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int d = 32 * dt + 8 * i + 4 * hh;
+          const int d = 32 * dt + 8 * i + 4 * hh_o;
           st_bf16x4(orow + d, oacc[dt][4 * i] * inv, oacc[dt][4 * i + 1] * inv,
                     oacc[dt][4 * i + 2] * inv, oacc[dt][4 * i + 3] * inv);
         }
-      if (a.lse != nullptr && hh == 0)
-        a.lse[(int64_t)(sd.q_start + tok) * a.Hq + head] = lse2 * 0.69314718055994531f;
+      if (a.lse != nullptr && hh_o == 0)
+        a.lse[(int64_t)(sd.q_start + o_tok) * a.Hq + o_head] = lse2 * 0.69314718055994531f;
     }
   } else {
-    const int lrow = wave * 32 + (lane & 31);
+    const int lrow = wave * 32 + (lane_o & 31);
     float* po = a.part_o + ((int64_t)it.part * kRows + lrow) * kHD;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int d = 32 * dt + 8 * i + 4 * hh;
+        const int d = 32 * dt + 8 * i + 4 * hh_o;
         f32x4 w = {oacc[dt][4 * i] * inv, oacc[dt][4 * i + 1] * inv, oacc[dt][4 * i + 2] * inv,
                    oacc[dt][4 * i + 3] * inv};
         *(f32x4*)(po + d) = w;
       }
-    if (hh == 0) a.part_lse[(int64_t)it.part * kRows + lrow] = lse2;
+    if (hh_o == 0) a.part_lse[(int64_t)it.part * kRows + lrow] = lse2;
   }
 }
 
