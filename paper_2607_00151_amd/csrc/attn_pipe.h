@@ -310,16 +310,31 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
     float ls = 0.f;
     if (wave_active) {
       if (has_next) {
+        // operand reads two MFMAs ahead, P(t) between the MFMAs
+        bf16x8 kop[16];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) s_step(sc[1], read_k(kb, i), i);
+        for (int i = 0; i < 2; ++i) kop[i] = read_k(kb, i);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          if (i + 2 < 16) kop[i + 2] = read_k(kb, i + 2);
+          s_step(sc[1], kop[i], i);
+          ls += exp_pair(sc[0], i);
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) ls += exp_pair(sc[0], j);
       }
-#pragma unroll
-      for (int j = 0; j < 16; ++j) ls += exp_pair(sc[0], j);
     }
     if constexpr (kGroups == 2) lds_barrier();
     if (wave_active) {
+      bf16x8 vop[16];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) pv_step(read_v(vb, i), i);
+      for (int i = 0; i < 2; ++i) vop[i] = read_v(vb, i);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        if (i + 2 < 16) vop[i + 2] = read_v(vb, i + 2);
+        pv_step(vop[i], i);
+      }
       l += ls;
       if (has_next) {
         if ((t + 2) * kKT > w_full) mask_tile(t + 1, sc[1]);
@@ -466,13 +481,13 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
     for (int j = 0; j < kPagesPerTile; ++j) s_b.s[j] = (int32_t)__builtin_amdgcn_readfirstlane(v_next[j]);
     v_next = fetch_vec(t + 3);
   };
-  // Steps t < t_fast interleave: their next tile needs no mask and the
-  // tiles they load, K(t+2) and V(t+1), are full and covered by an intact
-  // table.  Waves run different numbers of each kind of step but the same
-  // number of steps, each with one barrier and its share of the tile loads.
-  const int t_fast = (wave_active && table_ok)
-                         ? max(t0, min(min(t1 - 1, w_full / kKT - 1), it.kv_end / kKT - 2))
-                         : t0;
+  // Steps t < t_fast interleave: their next tile needs no mask, V(t+1) is a
+  // full tile and K(t+2) a tile of the item (the last one may be partial: its
+  // rows past the end are whatever the page holds, and the step that scores
+  // them masks them), all covered by an intact table.  Waves run different
+  // numbers of each kind of step but the same number of steps, each with one
+  // barrier and its share of the tile loads.
+  const int t_fast = (wave_active && table_ok) ? max(t0, min(w_full / kKT - 1, t1 - 2)) : t0;
   int t = t0;
   for (; t + 1 < t_fast; t += 2) {
     priority(t);
