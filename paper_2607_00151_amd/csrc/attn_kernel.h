@@ -50,6 +50,9 @@ struct AttnItem {
   int32_t kv_end;    // one past the last key this item reads (<= kv_len)
   int32_t part;      // -1: final output; else index of this item's partial slot
   int32_t boost;     // steps at the start that run at raised wave priority (0: none)
+  int32_t q_start;   // the sequence's SeqDesc fields, repeated so that one read
+  int32_t q_len;     // of the item gives a workgroup all it needs to start
+  int32_t kv_len;
 };
 
 struct SeqDesc {

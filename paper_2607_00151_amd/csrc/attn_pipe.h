@@ -49,16 +49,36 @@ struct PipeLds {
 };
 
 // Page slots of an item are checked once: true if every page its keys need is
-// present and in range.  Every thread of the block takes part (one barrier).
+// present and in range.  The first round of reads (four per thread, enough
+// for an item of up to 4 x nthreads pages) is issued early and evaluated
+// later, so its latency overlaps the first tile loads; every thread of the
+// block takes part in the evaluation (one barrier).
+struct TableCheck {
+  int32_t v[4];
+  int pg, pg_end;
+  bool bad;
+};
+
 template <int P>
-__device__ __forceinline__ bool item_table_ok(const AttnArgs& a, const AttnItem& it, int nthreads) {
+__device__ __forceinline__ TableCheck table_check_issue(const AttnArgs& a, const AttnItem& it, int32_t pt_base,
+                                                        int32_t pt_count, int nthreads) {
   constexpr int kPagesPerTile = kKT / P;
-  const int32_t pt_base = ld_uniform(a.indptr + it.seq);
-  const int32_t pt_count = ld_uniform(a.indptr + it.seq + 1) - pt_base;
   const int t0 = it.kv_begin / kKT;
   const int t1 = (it.kv_end + kKT - 1) / kKT;
-  bool bad = pt_count < (it.kv_end + P - 1) / P;
-  for (int pg = t0 * kPagesPerTile + (int)threadIdx.x; pg < min(t1 * kPagesPerTile, pt_count); pg += nthreads) {
+  TableCheck c;
+  c.bad = pt_count < (it.kv_end + P - 1) / P;
+  c.pg = t0 * kPagesPerTile + (int)threadIdx.x;
+  c.pg_end = min(t1 * kPagesPerTile, pt_count);
+#pragma unroll
+  for (int u = 0; u < 4; ++u) c.v[u] = c.pg + u * nthreads < c.pg_end ? a.indices[pt_base + c.pg + u * nthreads] : 0;
+  return c;
+}
+
+__device__ __forceinline__ bool table_check_finish(const AttnArgs& a, TableCheck& c, int32_t pt_base, int nthreads) {
+  bool bad = c.bad;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) bad |= !(c.v[u] >= 0 && c.v[u] < a.num_slots);
+  for (int pg = c.pg + 4 * nthreads; pg < c.pg_end; pg += nthreads) {
     const int32_t s = a.indices[pt_base + pg];
     bad |= !(s >= 0 && s < a.num_slots);
   }
@@ -114,19 +134,18 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
   const bool wave_active = wrow0 < rows_total;
   const int w_full = min(g_hi, pre + wrow0 / G + 1);         // keys below are visible to all rows
 
+  // the query row; it is scaled by c (below) only once the first tiles and
+  // the page-table check are under way, so its load latency overlaps theirs
   bf16x8 qop[8];             // c q, rounded to bf16
   {
     const uint16_t* qrow = a.q + ((int64_t)(sd.q_start + tok) * a.Hq + head) * kHD;
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) {
-      const bf16x8 raw = ld_bf16x8(qrow + (2 * ks + hh) * 8);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qop[ks][e] = (__bf16)((float)raw[e] * a.c);
-    }
+    for (int ks = 0; ks < 8; ++ks) qop[ks] = ld_bf16x8(qrow + (2 * ks + hh) * 8);
   }
 
   const int32_t pt_base = ld_uniform(a.indptr + it.seq);
   const int32_t pt_count = ld_uniform(a.indptr + it.seq + 1) - pt_base;
+  TableCheck tcheck = table_check_issue<P>(a, it, pt_base, pt_count, 64 * WAVES * kGroups);
   const int64_t slot_bytes = (int64_t)a.Hkv * P * kHD * 2;
   const char* kbase = (const char*)a.k;
   const char* vbase = (const char*)a.v;
@@ -441,7 +460,11 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
       return __builtin_bit_cast(slot_vec, __builtin_amdgcn_raw_buffer_load_b64(rsrc_pt, t * 8, 0, 0));
   };
   slot_vec v_next = fetch_vec(t0 + 2);                      // pages of tile t + 2, in flight
-  table_ok = item_table_ok<P>(a, it, 64 * WAVES * kGroups);
+  table_ok = table_check_finish(a, tcheck, pt_base, 64 * WAVES * kGroups);
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) qop[ks][e] = (__bf16)((float)qop[ks][e] * a.c);
   __builtin_amdgcn_s_waitcnt(0x0070);
   lds_barrier();
   if (kGroups == 2 && GRP == 1) lds_barrier();             // group 1 runs a barrier behind
@@ -617,7 +640,7 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t v_lds0[kTileBytes], v_lds1[kTileBytes];
   const AttnItem it = ld_uniform(a.items + blockIdx.x);
   if (it.kv_begin >= it.kv_end) return;                     // padding item
-  const SeqDesc sd = ld_uniform(a.seqs + it.seq);
+  const SeqDesc sd{it.q_start, it.q_len, it.kv_len, 0};
   const PipeLds L{(lds_u8*)k_lds0, (lds_u8*)k_lds1, (lds_u8*)v_lds0, (lds_u8*)v_lds1,
                   nullptr, nullptr, nullptr, nullptr, nullptr};
   pipe_group<P, kPoolRsrc, 1, 0>(a, it, sd, L);
@@ -634,7 +657,7 @@ __global__ __launch_bounds__(512, 1) void attn_pp_kernel(AttnArgs a) {
   __shared__ float ml[4 * kPipeRows];
   const AttnItem it = ld_uniform(a.items + blockIdx.x);
   if (it.kv_begin >= it.kv_end) return;                     // padding item
-  const SeqDesc sd = ld_uniform(a.seqs + it.seq);
+  const SeqDesc sd{it.q_start, it.q_len, it.kv_len, 0};
   lds_u8* const xb0 = (lds_u8*)k_b0;
   lds_u8* const xb1 = (lds_u8*)k_b1;
   lds_u8* const xb2 = (lds_u8*)v_b0;

@@ -551,6 +551,12 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
     for (const Work& w : work) items.push_back(w.it);
     pair_rounds(items, (size_t)ctx->num_cu);
   }
+  for (sa::AttnItem& x : items) {
+    if (x.kv_end <= x.kv_begin) continue;              // padding
+    x.q_start = seqs[x.seq].q_start;
+    x.q_len = seqs[x.seq].q_len;
+    x.kv_len = seqs[x.seq].kv_len;
+  }
   // Finishing a CU's two blocks together.  Of two co-resident blocks the
   // older (first-round) one wins the SIMD's issue arbitration: measured at
   // c2, the favoured block advances at about 1.4 times the other's rate
