@@ -410,32 +410,42 @@ struct MergeArgs {
   int32_t rows;              // rows per work item
 };
 
+// grid: x = merge group, y = 32-row slice of the group's rows.  Thread
+// (row, c) of a block merges 16 consecutive d of one row: every partial's
+// 64-byte piece of that row is read with four 16-byte loads, the LSE of the
+// row once per partial.
 __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
   const MergeGroup g = a.groups[blockIdx.x];
   const SeqDesc sd = a.seqs[g.seq];
   const int rows_total = sd.q_len * a.G;
-  for (int idx = threadIdx.x; idx < a.rows * kHD; idx += 256) {
-    const int lrow = idx / kHD, d = idx % kHD;
-    const int r = g.row0 + lrow;
-    if (r >= rows_total) continue;
-    float mx = -INFINITY;
-    for (int s = 0; s < g.nsplit; ++s) mx = fmaxf(mx, a.part_lse[(int64_t)(g.part0 + s) * a.rows + lrow]);
-    float num = 0.f, den = 0.f;
-    if (mx != -INFINITY) {
-      for (int s = 0; s < g.nsplit; ++s) {
-        const int64_t p = (int64_t)(g.part0 + s) * a.rows + lrow;
-        const float w = exp2f_fast(a.part_lse[p] - mx);
-        den += w;
-        num += w * a.part_o[p * kHD + d];
-      }
+  const int lrow = blockIdx.y * 32 + (threadIdx.x >> 3);
+  const int d0 = (threadIdx.x & 7) * 16;
+  const int r = g.row0 + lrow;
+  if (lrow >= a.rows || r >= rows_total) return;
+  float mx = -INFINITY;
+  for (int s = 0; s < g.nsplit; ++s) mx = fmaxf(mx, a.part_lse[(int64_t)(g.part0 + s) * a.rows + lrow]);
+  f32x4 num[4] = {};
+  float den = 0.f;
+  if (mx != -INFINITY) {
+#pragma unroll 2
+    for (int s = 0; s < g.nsplit; ++s) {
+      const int64_t p = (int64_t)(g.part0 + s) * a.rows + lrow;
+      const float w = exp2f_fast(a.part_lse[p] - mx);
+      const f32x4* src = (const f32x4*)(a.part_o + p * kHD + d0);
+      den += w;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) num[c] += w * src[c];
     }
-    const int tok = r / a.G;
-    const int head = g.kvh * a.G + (r - tok * a.G);
-    const int64_t orow = (int64_t)(sd.q_start + tok) * a.Hq + head;
-    a.o[orow * kHD + d] = f32_to_bf16_rne(den > 0.f ? num / den : 0.f);
-    if (a.lse != nullptr && d == 0)
-      a.lse[orow] = den > 0.f ? (mx + __builtin_amdgcn_logf(den)) * 0.69314718055994531f : -INFINITY;
   }
+  const float inv = den > 0.f ? 1.f / den : 0.f;
+  const int tok = r / a.G;
+  const int head = g.kvh * a.G + (r - tok * a.G);
+  const int64_t orow = (int64_t)(sd.q_start + tok) * a.Hq + head;
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+    st_bf16x4(a.o + orow * kHD + d0 + 4 * c, num[c][0] * inv, num[c][1] * inv, num[c][2] * inv, num[c][3] * inv);
+  if (a.lse != nullptr && d0 == 0)
+    a.lse[orow] = den > 0.f ? (mx + __builtin_amdgcn_logf(den)) * 0.69314718055994531f : -INFINITY;
 }
 
 }  // namespace sa

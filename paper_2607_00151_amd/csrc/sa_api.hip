@@ -492,10 +492,15 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
         total_tiles += tiles;
       }
   }
-  // split long items when there are too few to fill the chip
+  // Split long items by key range when there are too few to fill the chip:
+  // always below one item per CU; below two per CU (both workgroup slots of
+  // a CU) only when items average >= 128 key tiles, where the pairing gains
+  // more than the partial-merge launch costs (measured: a CU's two blocks
+  // together run ~1.3x one alone; the merge adds ~10-15 us).
   std::vector<sa::MergeGroup> groups;
   int32_t n_parts = 0;
-  if ((int64_t)work.size() < ctx->num_cu) {
+  const int64_t n_work = (int64_t)work.size();
+  if (n_work < ctx->num_cu || (n_work < 2 * ctx->num_cu && total_tiles >= 128 * n_work)) {
     const int64_t chunk = std::max<int64_t>(16, (total_tiles + 2 * ctx->num_cu - 1) / (2 * ctx->num_cu));
     std::vector<Work> split;
     for (const Work& w : work) {
@@ -632,7 +637,7 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
     m.Hq = Hq;
     m.G = G;
     m.rows = rows_item;
-    hipLaunchKernelGGL(sa::merge_kernel, dim3((unsigned)groups.size()), dim3(256), 0,
+    hipLaunchKernelGGL(sa::merge_kernel, dim3((unsigned)groups.size(), (unsigned)((rows_item + 31) / 32)), dim3(256), 0,
                        (hipStream_t)stream, m);
     SA_HIP(hipGetLastError());
   }
