@@ -168,6 +168,31 @@ sa_status sa_kv_assemble(sa_ctx *ctx, const sa_layout *layout,
                          int32_t *h_dst_len, void *stream);
 
 /*
+ * sa_kv_splice_alias — zero-copy form of the commit splice (paper Sec. 3.2
+ * commit, Sec. 3.4 keep-recent-K), for callers whose surviving pages may stay
+ * where they are.
+ *
+ * Same spans, lengths, free list and outputs as sa_kv_assemble, but no page
+ * is copied: the destination table of sequence b lists the SOURCE slots of its
+ * surviving pages, in order, followed by fresh slots -- taken from the front of
+ * d_fresh, sequence after sequence -- for the pages that h_reserve[b] more
+ * tokens need beyond the surviving ones (so the free list is consumed only by
+ * reserved pages).  The surviving pages are then shared between the source and
+ * the destination tables: an append into the last surviving page (when it is
+ * partial) writes into the source slot, past the source's own length.
+ *
+ * Errors: as sa_kv_assemble (d_fresh may be NULL when no page is reserved).
+ * A missing source page or a source slot outside [0, num_slots) is latched in
+ * the device flag that sa_sync_check reports (a missing page's entry is -1).
+ */
+sa_status sa_kv_splice_alias(sa_ctx *ctx, const sa_layout *layout, int32_t batch,
+                             const int32_t *h_src_len, const int32_t *h_keep_indptr,
+                             const int32_t *h_keep_spans, const int32_t *h_reserve,
+                             sa_pages src, const int32_t *d_fresh, int32_t num_fresh,
+                             int32_t *d_dst_indptr, int32_t *d_dst_indices, int32_t dst_capacity,
+                             int32_t *h_dst_len, void *stream);
+
+/*
  * sa_segment_prefill_attn — causal grouped-query attention of each
  * sequence's last h_q_len[b] tokens over its h_kv_len[b] cached tokens
  * (paper Sec. 4, prefill-attention term; decode rows are the q_len = 1 case of

@@ -122,6 +122,48 @@ def assemble(src_len, src_indptr, src_indices, keep_indptr, keep_spans, reserve,
     }
 
 
+def splice_alias(src_len, src_indptr, src_indices, keep_indptr, keep_spans, reserve, fresh, P):
+    """Zero-copy form of the splice: the replacement cache of a sequence is its
+    surviving source pages, in order, left in their source slots, followed by
+    as many new pages as ``reserve`` further tokens need, whose slots are taken
+    from the front of the free list, sequence after sequence.  Nothing is copied.
+
+    Returns dict with dst_indptr [B+1], dst_indices, dst_len [B] (kept tokens)
+    and fresh_used (free-list entries consumed).
+    """
+    B = len(src_len)
+    dst_indptr, dst_indices, dst_len = [0], [], []
+    cursor = 0
+    for b in range(B):
+        n_src_pages = pages_for(src_len[b], P)
+        if int(src_indptr[b + 1]) - int(src_indptr[b]) < n_src_pages:
+            raise ValueError(f"sequence {b}: page list shorter than its length")
+        kept_pages, prev_end = [], 0
+        for s in range(int(keep_indptr[b]), int(keep_indptr[b + 1])):
+            begin, end = int(keep_spans[s][0]), int(keep_spans[s][1])
+            if not (prev_end <= begin < end <= n_src_pages):
+                raise ValueError(f"sequence {b}: bad keep span [{begin}, {end})")
+            prev_end = end
+            kept_pages.extend(range(begin, end))
+        kept = sum(kept_tokens_of_page(src_len[b], p, P) for p in kept_pages)
+        n_dst = max(len(kept_pages), pages_for(kept + int(reserve[b]), P))
+        for p in kept_pages:
+            dst_indices.append(int(src_indices[int(src_indptr[b]) + p]))
+        n_new = n_dst - len(kept_pages)
+        if cursor + n_new > len(fresh):
+            raise ValueError("free list exhausted")
+        dst_indices.extend(int(x) for x in fresh[cursor: cursor + n_new])
+        cursor += n_new
+        dst_indptr.append(len(dst_indices))
+        dst_len.append(kept)
+    return {
+        "dst_indptr": np.asarray(dst_indptr, dtype=np.int32),
+        "dst_indices": np.asarray(dst_indices, dtype=np.int32),
+        "dst_len": np.asarray(dst_len, dtype=np.int64),
+        "fresh_used": cursor,
+    }
+
+
 def gather_logical(pool, indptr, indices, lengths, P, b):
     """Contiguous [len][Hkv][D] rows of sequence b read back through its page list."""
     n = int(lengths[b])

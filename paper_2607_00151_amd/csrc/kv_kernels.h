@@ -160,4 +160,42 @@ __global__ __launch_bounds__(kAsmThreads) void assemble_kernel(AsmArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- zero-copy splice
+
+struct AliasArgs {
+  const AsmUnit* units;        // surviving pages (sequence, source page)
+  const int32_t* entry;        // [n_dst] unit index, or -(fresh position + 1) for a reserved page
+  const int32_t* dst_indptr;   // [B + 1] plan copy of the destination table offsets
+  const int32_t* src_indptr;
+  const int32_t* src_indices;
+  const int32_t* fresh;
+  int32_t* out_indptr;
+  int32_t* out_indices;
+  int32_t* err;
+  int64_t num_slots;
+  int32_t n_dst, B;
+};
+
+// One thread per destination table entry: a surviving page's entry is its
+// source slot, a reserved page's entry the next fresh slot.  Nothing is copied.
+// A missing source page or a slot outside [0, num_slots) raises the error
+// flag (the entry is written as -1 for a missing page, as found otherwise).
+__global__ __launch_bounds__(256) void splice_alias_kernel(AliasArgs a) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e <= a.B) a.out_indptr[e] = a.dst_indptr[e];
+  if (e >= a.n_dst) return;
+  const int32_t code = a.entry[e];
+  int32_t slot;
+  if (code >= 0) {
+    const AsmUnit un = a.units[code];
+    const int32_t sbase = a.src_indptr[un.seq];
+    const int32_t scount = a.src_indptr[un.seq + 1] - sbase;
+    slot = un.src_page < scount ? a.src_indices[sbase + un.src_page] : -1;
+  } else {
+    slot = a.fresh[-code - 1];
+  }
+  if (slot < 0 || (int64_t)slot >= a.num_slots) atomicOr(a.err, 4);
+  a.out_indices[e] = slot;
+}
+
 }  // namespace sa

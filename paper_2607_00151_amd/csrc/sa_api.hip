@@ -57,7 +57,7 @@ struct PlanImage {
   }
 };
 
-enum PlanKind { kPlanAppend = 0, kPlanAssemble = 1, kPlanAttn = 2, kPlanKinds = 3 };
+enum PlanKind { kPlanAppend = 0, kPlanAssemble = 1, kPlanAttn = 2, kPlanAlias = 3, kPlanKinds = 4 };
 
 }  // namespace
 
@@ -335,13 +335,24 @@ sa_status sa_kv_append(sa_ctx* ctx, const sa_layout* layout, int32_t layer, void
 
 // ----------------------------------------------------------------- assemble
 
-sa_status sa_kv_assemble(sa_ctx* ctx, const sa_layout* layout, const void* k_src,
-                         const void* v_src, void* k_dst, void* v_dst, int32_t batch,
-                         const int32_t* h_src_len, const int32_t* h_keep_indptr,
-                         const int32_t* h_keep_spans, const int32_t* h_reserve, sa_pages src,
-                         const int32_t* d_fresh, int32_t num_fresh, int32_t* d_dst_indptr,
-                         int32_t* d_dst_indices, int32_t dst_capacity, int32_t* h_dst_len,
-                         void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Host plan of a commit splice: validated spans, one record per surviving
+// page, and the destination table's offsets.  With `alias`, surviving pages
+// keep their source slots and only the reserved pages take fresh slots.
+struct SplicePlan {
+  std::vector<sa::AsmUnit> units;      // surviving pages, in destination order
+  std::vector<int32_t> dst_indptr, dst_len;
+  std::vector<int32_t> entry;          // alias: per destination entry, unit index or -(fresh position + 1)
+  int64_t n_dst = 0, fresh_used = 0;
+};
+
+sa_status plan_splice(const sa_layout* layout, int32_t batch, const int32_t* h_src_len,
+                      const int32_t* h_keep_indptr, const int32_t* h_keep_spans, const int32_t* h_reserve,
+                      bool alias, int32_t num_fresh, int32_t dst_capacity, int32_t* h_dst_len,
+                      SplicePlan& out) {
   sa_status s = check_layout(layout);
   if (s != SA_OK) return s;
   if (batch < 1) return fail(SA_ERR_SHAPE, "batch %d < 1", batch);
@@ -351,9 +362,9 @@ sa_status sa_kv_assemble(sa_ctx* ctx, const sa_layout* layout, const void* k_src
   if (h_keep_indptr[batch] > 0 && !h_keep_spans) return fail(SA_ERR_NULL, "h_keep_spans is NULL");
   if (num_fresh < 0 || dst_capacity < 0) return fail(SA_ERR_SHAPE, "negative capacity");
   const int P = layout->page_size;
-  std::vector<sa::AsmUnit> unit_list;
-  std::vector<int32_t> dst_indptr(batch + 1, 0), dst_len(batch, 0);
-  int64_t units = 0, n_dst = 0;
+  out.dst_indptr.assign(batch + 1, 0);
+  out.dst_len.assign(batch, 0);
+  int64_t n_dst = 0, fresh_used = 0;
   for (int b = 0; b < batch; ++b) {
     if (h_src_len[b] < 0 || h_reserve[b] < 0)
       return fail(SA_ERR_SHAPE, "sequence %d: src_len %d, reserve %d", b, h_src_len[b], h_reserve[b]);
@@ -367,24 +378,54 @@ sa_status sa_kv_assemble(sa_ctx* ctx, const sa_layout* layout, const void* k_src
       if (beg < prev_end || beg >= end || end > n_src_pages)
         return fail(SA_ERR_RANGE, "sequence %d: keep span [%d, %d) invalid (previous end %d, %d pages)",
                     b, beg, end, prev_end, n_src_pages);
-      for (int p = beg; p < end; ++p)
-        unit_list.push_back({b, p, (int32_t)(n_dst + kept_pages + (p - beg))});
-      for (int p = beg; p < end; ++p) kept += std::min(P, h_src_len[b] - p * P);
+      for (int p = beg; p < end; ++p) {
+        if (alias) out.entry.push_back((int32_t)out.units.size());
+        out.units.push_back({b, p, (int32_t)(n_dst + kept_pages + (p - beg))});
+        kept += std::min(P, h_src_len[b] - p * P);
+      }
       kept_pages += end - beg;
-      units += end - beg;
       prev_end = end;
     }
     const int64_t pages_b = std::max<int64_t>(kept_pages, (kept + h_reserve[b] + P - 1) / P);
-    dst_len[b] = (int32_t)kept;
+    const int64_t fresh_b = alias ? pages_b - kept_pages : pages_b;
+    if (alias)
+      for (int64_t j = 0; j < fresh_b; ++j) out.entry.push_back((int32_t)(-(fresh_used + j) - 1));
+    out.dst_len[b] = (int32_t)kept;
     n_dst += pages_b;
+    fresh_used += fresh_b;
     if (n_dst > INT32_MAX) return fail(SA_ERR_SHAPE, "destination table too large");
-    dst_indptr[b + 1] = (int32_t)n_dst;
+    out.dst_indptr[b + 1] = (int32_t)n_dst;
   }
-  if (n_dst > num_fresh)
-    return fail(SA_ERR_NO_PAGES, "need %lld fresh slots, %d given", (long long)n_dst, num_fresh);
+  if (fresh_used > num_fresh)
+    return fail(SA_ERR_NO_PAGES, "need %lld fresh slots, %d given", (long long)fresh_used, num_fresh);
   if (n_dst > dst_capacity)
     return fail(SA_ERR_NO_PAGES, "destination table needs %lld entries, capacity %d",
                 (long long)n_dst, dst_capacity);
+  out.n_dst = n_dst;
+  out.fresh_used = fresh_used;
+  return SA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+
+sa_status sa_kv_assemble(sa_ctx* ctx, const sa_layout* layout, const void* k_src,
+                         const void* v_src, void* k_dst, void* v_dst, int32_t batch,
+                         const int32_t* h_src_len, const int32_t* h_keep_indptr,
+                         const int32_t* h_keep_spans, const int32_t* h_reserve, sa_pages src,
+                         const int32_t* d_fresh, int32_t num_fresh, int32_t* d_dst_indptr,
+                         int32_t* d_dst_indices, int32_t dst_capacity, int32_t* h_dst_len,
+                         void* stream) {
+  SplicePlan sp;
+  sa_status s = plan_splice(layout, batch, h_src_len, h_keep_indptr, h_keep_spans, h_reserve, false,
+                            num_fresh, dst_capacity, h_dst_len, sp);
+  if (s != SA_OK) return s;
+  std::vector<sa::AsmUnit>& unit_list = sp.units;
+  std::vector<int32_t>& dst_indptr = sp.dst_indptr;
+  std::vector<int32_t>& dst_len = sp.dst_len;
+  const int64_t units = (int64_t)unit_list.size(), n_dst = sp.n_dst;
   if (!k_src || !v_src || !k_dst || !v_dst || !src.indptr || !src.indices || !d_fresh ||
       !d_dst_indptr || !d_dst_indices)
     return fail(SA_ERR_NULL, "a device pointer is NULL");
@@ -424,6 +465,49 @@ sa_status sa_kv_assemble(sa_ctx* ctx, const sa_layout* layout, const void* k_src
   const int64_t gx = std::max<int64_t>(units, table_blocks);
   hipLaunchKernelGGL(sa::assemble_kernel, dim3((unsigned)gx, (unsigned)layout->num_layers), dim3(sa::kAsmThreads),
                      0, (hipStream_t)stream, a);
+  SA_HIP(hipGetLastError());
+  return SA_OK;
+}
+
+sa_status sa_kv_splice_alias(sa_ctx* ctx, const sa_layout* layout, int32_t batch,
+                             const int32_t* h_src_len, const int32_t* h_keep_indptr,
+                             const int32_t* h_keep_spans, const int32_t* h_reserve, sa_pages src,
+                             const int32_t* d_fresh, int32_t num_fresh, int32_t* d_dst_indptr,
+                             int32_t* d_dst_indices, int32_t dst_capacity, int32_t* h_dst_len,
+                             void* stream) {
+  SplicePlan sp;
+  sa_status s = plan_splice(layout, batch, h_src_len, h_keep_indptr, h_keep_spans, h_reserve, true,
+                            num_fresh, dst_capacity, h_dst_len, sp);
+  if (s != SA_OK) return s;
+  if (!src.indptr || !src.indices || !d_dst_indptr || !d_dst_indices || (sp.fresh_used > 0 && !d_fresh))
+    return fail(SA_ERR_NULL, "a device pointer is NULL");
+  s = check_ctx(ctx);
+  if (s != SA_OK) return s;
+  memcpy(h_dst_len, sp.dst_len.data(), sizeof(int32_t) * batch);
+
+  PlanImage img;
+  const size_t o_un = img.add(sp.units.data(), sp.units.size());
+  const size_t o_ip = img.add(sp.dst_indptr.data(), sp.dst_indptr.size());
+  const size_t o_en = img.add(sp.entry.data(), sp.entry.size());
+  uint8_t* dev = nullptr;
+  s = upload_plan(ctx, kPlanAlias, img, (hipStream_t)stream, &dev);
+  if (s != SA_OK) return s;
+
+  sa::AliasArgs a{};
+  a.units = (const sa::AsmUnit*)(dev + o_un);
+  a.entry = (const int32_t*)(dev + o_en);
+  a.dst_indptr = (const int32_t*)(dev + o_ip);
+  a.src_indptr = src.indptr;
+  a.src_indices = src.indices;
+  a.fresh = d_fresh;
+  a.out_indptr = d_dst_indptr;
+  a.out_indices = d_dst_indices;
+  a.err = ctx->d_err;
+  a.num_slots = layout->num_slots;
+  a.n_dst = (int32_t)sp.n_dst;
+  a.B = batch;
+  const int64_t blocks = (std::max<int64_t>(sp.n_dst, batch + 1) + 255) / 256;
+  hipLaunchKernelGGL(sa::splice_alias_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, a);
   SA_HIP(hipGetLastError());
   return SA_OK;
 }

@@ -114,6 +114,31 @@ def test_assemble_validation(lib):
     assert assemble(lib, L, [-1], [0, 0], [], [0]) == 2
 
 
+def splice_alias(lib, L, src_len, keep_indptr, spans, reserve, num_fresh=100, cap=100, fresh=FAKE):
+    a = [np.asarray(x, dtype=np.int32) for x in (src_len, keep_indptr, np.asarray(spans).reshape(-1),
+                                                  reserve)]
+    out = np.zeros(len(a[0]), dtype=np.int32)
+    rc = lib.sa_kv_splice_alias(None, ctypes.byref(L), len(a[0]), a[0].ctypes.data, a[1].ctypes.data,
+                                a[2].ctypes.data if a[2].size else None, a[3].ctypes.data,
+                                sa._Pages(FAKE, FAKE), fresh, num_fresh, FAKE, FAKE, cap, out.ctypes.data,
+                                None)
+    return rc, out
+
+
+def test_splice_alias_validation(lib):
+    L = layout(page_size=16)
+    assert splice_alias(lib, L, [100], [0, 2], [[0, 2], [4, 7]], [10])[0] == 1   # host checks pass; no context
+    assert splice_alias(lib, L, [100], [0, 2], [[0, 2], [1, 7]], [10])[0] == 5   # overlap
+    assert splice_alias(lib, L, [100], [0, 1], [[0, 8]], [10])[0] == 5           # past the last page
+    # only reserved pages take fresh slots: 7 kept pages + 20 tokens -> 8 pages, 1 fresh
+    assert splice_alias(lib, L, [100], [0, 1], [[0, 7]], [20], num_fresh=1)[0] == 1
+    assert splice_alias(lib, L, [100], [0, 1], [[0, 7]], [20], num_fresh=0)[0] == 6
+    assert splice_alias(lib, L, [100], [0, 1], [[0, 7]], [20], cap=7)[0] == 6
+    assert splice_alias(lib, L, [100], [0, 1], [[0, 7]], [12], num_fresh=0, fresh=None)[0] == 1  # no page reserved
+    assert splice_alias(lib, L, [100], [0, 1], [[0, 7]], [20], fresh=None)[0] == 1   # a NULL list is caught later
+    assert splice_alias(lib, L, [100], [1, 1], [[0, 7]], [10])[0] == 2           # indptr[0] != 0
+
+
 def test_context_creation_without_gpu(lib):
     import torch
     if torch.cuda.is_available():

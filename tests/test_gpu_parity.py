@@ -229,21 +229,29 @@ def test_out_of_range_slot_is_reported(ctx):
 
 # ------------------------------------------------------ whole step, full size
 
-def run_step(ctx, w, L, state):
-    """assemble (commit splice) -> append (segment) -> attention, as timed by the bench."""
+def run_step(ctx, w, L, state, alias=False):
+    """assemble (commit splice; zero-copy with alias) -> append (segment) -> attention, as
+    timed by the bench."""
     kp, vp, sip, sid, fresh, dip, did, q, ks, vs, o, lse = state
     a = w.asm
-    dst_len = sa.sa_kv_assemble(ctx, L, kp, vp, kp, vp, a.src_len, a.keep_indptr, a.keep_spans,
-                                a.reserve, sip, sid, fresh, dip, did)
+    if alias:
+        dst_len = sa.sa_kv_splice_alias(ctx, L, a.src_len, a.keep_indptr, a.keep_spans, a.reserve, sip,
+                                        sid, fresh, dip, did)
+    else:
+        dst_len = sa.sa_kv_assemble(ctx, L, kp, vp, kp, vp, a.src_len, a.keep_indptr, a.keep_spans,
+                                    a.reserve, sip, sid, fresh, dip, did)
     sa.sa_kv_append(ctx, L, 0, kp, vp, ks, vs, dst_len, w.qlen, dip, did)
     sa.sa_segment_prefill_attn(ctx, L, 0, q, kp, vp, w.qlen, dst_len + w.qlen, dip, did, w.scale,
                                o, lse)
     return dst_len
 
 
-def check_step(ctx, w, per_seq_rows):
+def check_step(ctx, w, per_seq_rows, alias=False):
     L = layout_of(w)
     kp, vp, sip, sid, fresh = build_source_cache(w)
+    if alias:
+        # slots outside the source pages and the segment's pages must stay untouched
+        k_before, v_before = kp.clone(), vp.clone()
     n_dst = len(w.asm.fresh)
     dip = torch.zeros(w.batch + 1, dtype=torch.int32, device="cuda")
     did = torch.full((n_dst,), -1, dtype=torch.int32, device="cuda")
@@ -252,12 +260,21 @@ def check_step(ctx, w, per_seq_rows):
     lse = torch.empty((T, w.num_q_heads), dtype=torch.float32, device="cuda")
     state = (kp, vp, sip, sid, fresh, dip, did, dev_u16(w.q), dev_u16(w.k_seg()),
              dev_u16(w.v_seg()), o, lse)
-    dst_len = run_step(ctx, w, L, state)
+    dst_len = run_step(ctx, w, L, state, alias)
     sa.sa_sync_check(ctx)
     assert np.array_equal(dst_len, w.pre)
     # the assembled cache reads back as prefix ++ segment, bit for bit (sampled sequences)
-    r = opages.assemble(w.asm.src_len, w.asm.src_indptr, w.asm.src_indices, w.asm.keep_indptr,
-                        w.asm.keep_spans, w.asm.reserve, w.asm.fresh, w.page_size)
+    splice = opages.splice_alias if alias else opages.assemble
+    r = splice(w.asm.src_len, w.asm.src_indptr, w.asm.src_indices, w.asm.keep_indptr,
+               w.asm.keep_spans, w.asm.reserve, w.asm.fresh, w.page_size)
+    if alias:
+        # no page was copied: only the rows the segment was appended to changed
+        sl, ro = opages.append_destinations(w.pre, w.qlen, r["dst_indptr"], r["dst_indices"], w.page_size)
+        touched = torch.zeros((L.num_slots, w.page_size), dtype=torch.bool, device="cuda")
+        touched[torch.from_numpy(sl).cuda(), torch.from_numpy(ro).cuda()] = True
+        for after, before in ((kp, k_before), (vp, v_before)):
+            keep = ~touched[:, None, :, None].expand_as(after[0])
+            assert torch.equal(after[0][keep], before[0][keep])
     assert np.array_equal(dip.cpu().numpy(), r["dst_indptr"])
     assert np.array_equal(did.cpu().numpy()[: r["dst_indptr"][-1]], r["dst_indices"])
     ip_h, ix_h = r["dst_indptr"], r["dst_indices"]
@@ -283,6 +300,11 @@ def check_step(ctx, w, per_seq_rows):
 @pytest.mark.parametrize("name", WITH_ASM)
 def test_step_small(ctx, name):
     check_step(ctx, small(name), per_seq_rows=64)
+
+
+@pytest.mark.parametrize("name", WITH_ASM)
+def test_step_small_zero_copy_splice(ctx, name):
+    check_step(ctx, small(name), per_seq_rows=64, alias=True)
 
 
 @pytest.mark.timeout(600)

@@ -324,3 +324,43 @@ def test_assemble_rejects_overlapping_spans():
         pages.assemble([32], [0, 4], [0, 1, 2, 3], [0, 1], [(0, 5)], [0], [9, 8, 7, 6, 5], 8)
     with pytest.raises(ValueError):
         pages.assemble([32], [0, 4], [0, 1, 2, 3], [0, 1], [(0, 4)], [0], [9, 8, 7], 8)
+
+
+def test_alias_splice_reads_back_the_surviving_tokens_without_copying():
+    """The zero-copy splice: reading the replacement cache through its table
+    gives the source tokens with the dropped pages cut out, from the untouched
+    pool; its table is the copy splice's with every surviving entry replaced by
+    the page's source slot, and only reserved pages consume the free list."""
+    P, Hkv, D, S = 8, 2, 4, 200
+    src_len = [61, 16, 9, 30]
+    spans = [[(0, 2), (5, 8)], [(1, 2)], [(0, 2)], []]
+    reserve = [10, 0, 7, 3]
+    npg = [pages.pages_for(n, P) for n in src_len]
+    src_indptr = np.concatenate([[0], np.cumsum(npg)])
+    perm = rng.permutation(7, 0, S)
+    src_indices = perm[: src_indptr[-1]]
+    fresh = perm[src_indptr[-1]:]
+    keep_indptr = np.concatenate([[0], np.cumsum([len(s) for s in spans])])
+    keep_spans = [x for s in spans for x in s]
+    pool = rng.normal_bf16(7, 1, (S, Hkv, P, D))
+    before = pool.copy()
+    r = pages.splice_alias(src_len, src_indptr, src_indices, keep_indptr, keep_spans, reserve, fresh, P)
+    c = pages.assemble(src_len, src_indptr, src_indices, keep_indptr, keep_spans, reserve, fresh, P)
+    assert r["dst_indptr"].tolist() == c["dst_indptr"].tolist()
+    assert r["dst_len"].tolist() == c["dst_len"].tolist()
+    n_fresh = 0
+    for b in range(len(src_len)):
+        src = pages.gather_logical(pool, src_indptr[b:], src_indices, [src_len[b]], P, 0)
+        want = np.concatenate([src[p0 * P: min(p1 * P, src_len[b])] for p0, p1 in spans[b]]
+                              or [src[:0]])
+        got = pages.gather_logical(pool, r["dst_indptr"][b:], r["dst_indices"], [r["dst_len"][b]], P, 0)
+        assert np.array_equal(got, want)
+        kept_pages = [p for p0, p1 in spans[b] for p in range(p0, p1)]
+        ent = r["dst_indices"][r["dst_indptr"][b]: r["dst_indptr"][b + 1]].tolist()
+        assert ent[: len(kept_pages)] == [int(src_indices[src_indptr[b] + p]) for p in kept_pages]
+        assert ent[len(kept_pages):] == list(fresh[n_fresh: n_fresh + len(ent) - len(kept_pages)])
+        n_fresh += len(ent) - len(kept_pages)
+    assert r["fresh_used"] == n_fresh
+    assert np.array_equal(pool, before)
+    with pytest.raises(ValueError):
+        pages.splice_alias([32], [0, 4], [0, 1, 2, 3], [0, 2], [(0, 2), (1, 3)], [0], [9], 8)

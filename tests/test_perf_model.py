@@ -57,3 +57,14 @@ def test_token_model_is_blind_to_cached_context():
 
 def test_max_rel_error():
     assert abs(pm.max_rel_error([1.1, 2.0], [1.0, 2.0]) - 0.1) < 1e-12
+
+
+def test_segment_roofline_bound_switches_at_the_ridge():
+    from paper_2607_00151_amd import segments as sg
+    # q x G rows per KV head = FLOP per K/V byte; the bf16 ridge is 2516.6e12 / 8e12 = 315
+    for q, bound in ((16, "hbm"), (32, "hbm"), (256, "mfma"), (512, "mfma")):
+        flop, byt, t, rows = sg.attention_roofline(32, q, 8192, 32, 8)
+        assert rows == 4 * q
+        got = "hbm" if byt / (sg.PEAK_GBS * 1e9) > flop / (sg.PEAK_TFLOPS * 1e12) else "mfma"
+        assert got == bound, q
+        assert abs(flop - 4 * 128 * 32 * 32 * pm.prefill_pairs(q, 8192)) < 1e-3 * flop
