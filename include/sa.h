@@ -168,6 +168,33 @@ sa_status sa_kv_assemble(sa_ctx *ctx, const sa_layout *layout,
                          int32_t *h_dst_len, void *stream);
 
 /*
+ * sa_kv_assemble_append — sa_kv_assemble followed by the segment's
+ * sa_kv_append, in one launch (paper Sec. 3.2: the transformed KV is the
+ * spliced prefix plus the segment's rows).
+ *
+ * Arguments and results of sa_kv_assemble, plus: layer, the layer whose new
+ * rows are written; k_new / v_new, bf16 [sum h_new_len][num_kv_heads][head_dim];
+ * h_new_len[b] (host), the new tokens of sequence b, which go to logical
+ * positions h_dst_len[b] .. h_dst_len[b] + h_new_len[b] - 1 of its
+ * replacement cache (they must fit its pages: kept + new <= pages_b *
+ * page_size).  The pools end exactly as after the two calls in sequence: the
+ * rows of a partial last surviving page that the segment fills come from the
+ * new rows, the rest of that page from its source.
+ *
+ * Errors: those of sa_kv_assemble, and SA_ERR_SHAPE for a bad layer or new
+ * tokens that do not fit, SA_ERR_NULL for NULL new rows or h_new_len.
+ */
+sa_status sa_kv_assemble_append(sa_ctx *ctx, const sa_layout *layout,
+                                const void *k_src, const void *v_src, void *k_dst, void *v_dst,
+                                int32_t batch, const int32_t *h_src_len,
+                                const int32_t *h_keep_indptr, const int32_t *h_keep_spans,
+                                const int32_t *h_reserve,
+                                sa_pages src, const int32_t *d_fresh, int32_t num_fresh,
+                                int32_t *d_dst_indptr, int32_t *d_dst_indices, int32_t dst_capacity,
+                                int32_t *h_dst_len, int32_t layer, const void *k_new,
+                                const void *v_new, const int32_t *h_new_len, void *stream);
+
+/*
  * sa_kv_splice_alias — zero-copy form of the commit splice (paper Sec. 3.2
  * commit, Sec. 3.4 keep-recent-K), for callers whose surviving pages may stay
  * where they are.

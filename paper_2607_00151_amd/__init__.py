@@ -14,7 +14,8 @@ import numpy as np
 
 __all__ = [
     "Layout", "Context", "SaError", "library_path", "load_library",
-    "sa_kv_append", "sa_kv_assemble", "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_sync_check",
+    "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append", "sa_kv_splice_alias",
+    "sa_segment_prefill_attn", "sa_sync_check",
     "EXPORTED_SYMBOLS",
 ]
 
@@ -23,8 +24,8 @@ _LIB_PATH = os.path.join(_PKG, "libsa.so")
 _lib = None
 
 EXPORTED_SYMBOLS = ("sa_create", "sa_destroy", "sa_status_string", "sa_last_error",
-                    "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_splice_alias",
-                    "sa_segment_prefill_attn")
+                    "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
+                    "sa_kv_splice_alias", "sa_segment_prefill_attn")
 
 STATUS = {0: "SA_OK", 1: "SA_ERR_NULL", 2: "SA_ERR_SHAPE", 3: "SA_ERR_UNSUPPORTED",
           4: "SA_ERR_ALIGN", 5: "SA_ERR_RANGE", 6: "SA_ERR_NO_PAGES", 7: "SA_ERR_HIP",
@@ -73,11 +74,13 @@ def load_library():
     lib.sa_kv_append.argtypes = [P, LP, I32, P, P, P, P, I32, P, P, _Pages, P]
     lib.sa_kv_assemble.argtypes = [P, LP, P, P, P, P, I32, P, P, P, P, _Pages, P, I32, P, P, I32,
                                    P, P]
+    lib.sa_kv_assemble_append.argtypes = [P, LP, P, P, P, P, I32, P, P, P, P, _Pages, P, I32, P, P, I32,
+                                          P, I32, P, P, P, P]
     lib.sa_kv_splice_alias.argtypes = [P, LP, I32, P, P, P, P, _Pages, P, I32, P, P, I32, P, P]
     lib.sa_segment_prefill_attn.argtypes = [P, LP, I32, P, P, P, I32, P, P, _Pages, ctypes.c_float,
                                             P, P, P]
-    for name in ("sa_create", "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_splice_alias",
-                 "sa_segment_prefill_attn"):
+    for name in ("sa_create", "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
+                 "sa_kv_splice_alias", "sa_segment_prefill_attn"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -190,6 +193,27 @@ def sa_kv_assemble(ctx, layout: Layout, k_src, v_src, k_dst, v_dst, src_len, kee
         _ptr(reserve), _pages(src_indptr, src_indices), _ptr(fresh), int(fresh.numel()),
         _ptr(dst_indptr), _ptr(dst_indices), int(dst_indices.numel()), _ptr(dst_len),
         _stream(stream)))
+    return dst_len
+
+
+def sa_kv_assemble_append(ctx, layout: Layout, k_src, v_src, k_dst, v_dst, src_len, keep_indptr,
+                          keep_spans, reserve, src_indptr, src_indices, fresh, dst_indptr, dst_indices,
+                          layer, k_new, v_new, new_len, stream=None):
+    """Splice and the segment's append in one launch.  Returns the kept token
+    count of every sequence (numpy int32); the new rows follow it."""
+    src_len, reserve, new_len = _host_i32(src_len), _host_i32(reserve), _host_i32(new_len)
+    keep_indptr = _host_i32(keep_indptr)
+    keep_spans = _host_i32(np.asarray(keep_spans).reshape(-1))
+    B = len(src_len)
+    if len(reserve) != B or len(keep_indptr) != B + 1 or len(new_len) != B:
+        raise ValueError("per-sequence arrays disagree on the batch size")
+    dst_len = np.zeros(B, dtype=np.int32)
+    _check(load_library().sa_kv_assemble_append(
+        _ctx_handle(ctx), ctypes.byref(layout), _ptr(k_src), _ptr(v_src), _ptr(k_dst), _ptr(v_dst),
+        B, _ptr(src_len), _ptr(keep_indptr), _ptr(keep_spans) if keep_spans.size else None,
+        _ptr(reserve), _pages(src_indptr, src_indices), _ptr(fresh), int(fresh.numel()),
+        _ptr(dst_indptr), _ptr(dst_indices), int(dst_indices.numel()), _ptr(dst_len), int(layer),
+        _ptr(k_new), _ptr(v_new), _ptr(new_len), _stream(stream)))
     return dst_len
 
 

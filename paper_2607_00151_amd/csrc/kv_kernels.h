@@ -72,6 +72,10 @@ struct AsmUnit {
   int32_t seq;
   int32_t src_page;
   int32_t dst_index;
+  // with an append in the same launch: rows app_row0 .. app_row0 + app_rows - 1
+  // of this page (the last surviving one, when partial) come from new-row
+  // token app_tok onwards instead of from the source page
+  int32_t app_row0, app_rows, app_tok;
 };
 
 struct AsmArgs {
@@ -91,6 +95,18 @@ struct AsmArgs {
   int64_t slot_elems;          // Hkv * P * 128
   int64_t layer_elems;         // num_slots * slot_elems
   int32_t n_units, n_dst, B;
+  // append of a segment in the same launch (app_layer < 0: none).  Blocks
+  // 0 .. app_blocks - 1 of that layer write the new rows that land on fresh
+  // pages (they go first: their address chains are the longest); blocks
+  // app_blocks .. app_blocks + n_units - 1 copy pages.  Tokens are listed per
+  // sequence like the append plan:
+  const uint16_t* k_new;       // [sum new][Hkv][128]
+  const uint16_t* v_new;
+  const int32_t* app_tok_begin;  // [B + 1] first listed token of each sequence
+  const int32_t* app_start;      // [B] its logical position in the replacement cache
+  const int32_t* app_knew;       // [B] its row in k_new / v_new
+  int64_t app_chunks;            // listed tokens * Hkv * 16
+  int32_t app_layer, app_blocks, Hkv, P;
 };
 
 constexpr int kAsmThreads = 512;
@@ -105,13 +121,51 @@ __device__ __forceinline__ void st_stream(uint16_t* p, u32x4 v) {
   __builtin_nontemporal_store(v, (u32x4*)p);
 }
 
-// grid: x = max(units, table blocks), y = layer.  One block of 512 threads
+// One page pair, kAsmDepth chunks of K and of V in flight per thread.  kMix:
+// the partial last surviving page of an append, whose rows
+// [app_row0, app_row0 + app_rows) are taken from the new rows instead.
+template <bool kMix>
+__device__ __forceinline__ void copy_page(const AsmArgs& a, const AsmUnit& un, const uint16_t* ks,
+                                          const uint16_t* vs, uint16_t* kd, uint16_t* vd, int tid) {
+  const int n_chunks = (int)(a.slot_elems / 8);
+  for (int base = 0; base < n_chunks; base += kAsmThreads * kAsmDepth) {
+    u32x4 kx[kAsmDepth], vx[kAsmDepth];
+#pragma unroll
+    for (int j = 0; j < kAsmDepth; ++j) {
+      const int c = base + j * kAsmThreads + tid;
+      if (c < n_chunks) {
+        const uint16_t* kp = ks + c * 8;
+        const uint16_t* vp = vs + c * 8;
+        if (kMix) {
+          const int g = c / (a.P * 16), r = (c >> 4) % a.P - un.app_row0;
+          if (r >= 0 && r < un.app_rows) {
+            const int64_t src = ((int64_t)(un.app_tok + r) * a.Hkv + g) * 128 + (c & 15) * 8;
+            kp = a.k_new + src;
+            vp = a.v_new + src;
+          }
+        }
+        kx[j] = ld_stream(kp);
+        vx[j] = ld_stream(vp);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kAsmDepth; ++j) {
+      const int c = base + j * kAsmThreads + tid;
+      if (c < n_chunks) {
+        st_stream(kd + c * 8, kx[j]);
+        st_stream(vd + c * 8, vx[j]);
+      }
+    }
+  }
+}
+
+// grid: x = max(app_blocks + units, table blocks), y = layer.  One block of 512 threads
 // copies one page of one layer, slot_elems * 2 bytes of K and as many of V,
 // with every chunk of a 32 KiB page pair in flight at once (512 threads were
 // measured ~4% faster than 256 for this copy on MI355X).  A unit's slots take
 // two dependent reads: its source page-table offset, then the slot.
 __global__ __launch_bounds__(kAsmThreads) void assemble_kernel(AsmArgs a) {
-  const int u = blockIdx.x;
+  int u = blockIdx.x;
   const int layer = blockIdx.y;
   const int tid = threadIdx.x;
 
@@ -121,6 +175,48 @@ __global__ __launch_bounds__(kAsmThreads) void assemble_kernel(AsmArgs a) {
     if (idx < a.n_dst) a.out_indices[idx] = a.fresh[idx];
     if (idx <= a.B) a.out_indptr[idx] = a.dst_indptr[idx];
   }
+  if (u < a.app_blocks) {
+    if (layer != a.app_layer) return;
+    // append: new rows onto fresh pages (the destination table is the free list
+    // in order, so the slot comes from it, not from the table being written).
+    // All addresses are resolved first, then every load is issued, then every
+    // store, so no chunk waits behind another chunk's store.
+    const int per_tok = a.Hkv * 16;
+    const int64_t lo = (int64_t)layer * a.layer_elems;
+    int64_t src[kAsmDepth], dst[kAsmDepth];
+#pragma unroll
+    for (int j = 0; j < kAsmDepth; ++j) {
+      const int64_t c = ((int64_t)u * kAsmDepth + j) * kAsmThreads + tid;
+      src[j] = -1;
+      if (c >= a.app_chunks) continue;
+      const int t = (int)(c / per_tok);
+      const int rem = (int)(c - (int64_t)t * per_tok);
+      const int g = rem >> 4, ch = rem & 15;
+      const int b = find_seq(a.app_tok_begin, a.B, t);
+      const int x = a.app_start[b] + (t - a.app_tok_begin[b]);
+      const int page = x / a.P, row = x - page * a.P;
+      if (page >= a.dst_indptr[b + 1] - a.dst_indptr[b]) { atomicOr(a.err, 2); continue; }
+      const int32_t slot = a.fresh[a.dst_indptr[b] + page];
+      if (slot < 0 || (int64_t)slot >= a.num_slots) { atomicOr(a.err, 2); continue; }
+      src[j] = ((int64_t)(a.app_knew[b] + (t - a.app_tok_begin[b])) * a.Hkv + g) * 128 + ch * 8;
+      dst[j] = lo + (((int64_t)slot * a.Hkv + g) * a.P + row) * 128 + ch * 8;
+    }
+    u32x4 kx[kAsmDepth], vx[kAsmDepth];
+#pragma unroll
+    for (int j = 0; j < kAsmDepth; ++j)
+      if (src[j] >= 0) {
+        kx[j] = ld_stream(a.k_new + src[j]);
+        vx[j] = ld_stream(a.v_new + src[j]);
+      }
+#pragma unroll
+    for (int j = 0; j < kAsmDepth; ++j)
+      if (src[j] >= 0) {
+        st_stream(a.k_dst + dst[j], kx[j]);
+        st_stream(a.v_dst + dst[j], vx[j]);
+      }
+    return;
+  }
+  u -= a.app_blocks;
   if (u >= a.n_units) return;
 
   const AsmUnit un = a.units[u];
@@ -138,26 +234,10 @@ __global__ __launch_bounds__(kAsmThreads) void assemble_kernel(AsmArgs a) {
   const uint16_t* vs = a.v_src + lo_off + (int64_t)s_slot * a.slot_elems;
   uint16_t* kd = a.k_dst + lo_off + (int64_t)d_slot * a.slot_elems;
   uint16_t* vd = a.v_dst + lo_off + (int64_t)d_slot * a.slot_elems;
-  const int n_chunks = (int)(a.slot_elems / 8);
-  for (int base = 0; base < n_chunks; base += kAsmThreads * kAsmDepth) {
-    u32x4 kx[kAsmDepth], vx[kAsmDepth];
-#pragma unroll
-    for (int j = 0; j < kAsmDepth; ++j) {
-      const int c = base + j * kAsmThreads + tid;
-      if (c < n_chunks) {
-        kx[j] = ld_stream(ks + c * 8);
-        vx[j] = ld_stream(vs + c * 8);
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < kAsmDepth; ++j) {
-      const int c = base + j * kAsmThreads + tid;
-      if (c < n_chunks) {
-        st_stream(kd + c * 8, kx[j]);
-        st_stream(vd + c * 8, vx[j]);
-      }
-    }
-  }
+  if (layer == a.app_layer && un.app_rows > 0)
+    copy_page<true>(a, un, ks, vs, kd, vd, tid);
+  else
+    copy_page<false>(a, un, ks, vs, kd, vd, tid);
 }
 
 // ---------------------------------------------------------------- zero-copy splice

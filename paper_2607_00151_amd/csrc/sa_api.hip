@@ -411,13 +411,18 @@ sa_status plan_splice(const sa_layout* layout, int32_t batch, const int32_t* h_s
 extern "C" {
 
 
-sa_status sa_kv_assemble(sa_ctx* ctx, const sa_layout* layout, const void* k_src,
-                         const void* v_src, void* k_dst, void* v_dst, int32_t batch,
-                         const int32_t* h_src_len, const int32_t* h_keep_indptr,
-                         const int32_t* h_keep_spans, const int32_t* h_reserve, sa_pages src,
-                         const int32_t* d_fresh, int32_t num_fresh, int32_t* d_dst_indptr,
-                         int32_t* d_dst_indices, int32_t dst_capacity, int32_t* h_dst_len,
-                         void* stream) {
+}  // extern "C"
+
+namespace {
+
+// The copy splice, and with new_len non-NULL an append of new rows of layer
+// `layer` behind each sequence's kept tokens in the same launch.
+sa_status splice_launch(sa_ctx* ctx, const sa_layout* layout, const void* k_src, const void* v_src,
+                        void* k_dst, void* v_dst, int32_t batch, const int32_t* h_src_len,
+                        const int32_t* h_keep_indptr, const int32_t* h_keep_spans, const int32_t* h_reserve,
+                        sa_pages src, const int32_t* d_fresh, int32_t num_fresh, int32_t* d_dst_indptr,
+                        int32_t* d_dst_indices, int32_t dst_capacity, int32_t* h_dst_len, int32_t layer,
+                        const void* k_new, const void* v_new, const int32_t* h_new_len, void* stream) {
   SplicePlan sp;
   sa_status s = plan_splice(layout, batch, h_src_len, h_keep_indptr, h_keep_spans, h_reserve, false,
                             num_fresh, dst_capacity, h_dst_len, sp);
@@ -426,6 +431,43 @@ sa_status sa_kv_assemble(sa_ctx* ctx, const sa_layout* layout, const void* k_src
   std::vector<int32_t>& dst_indptr = sp.dst_indptr;
   std::vector<int32_t>& dst_len = sp.dst_len;
   const int64_t units = (int64_t)unit_list.size(), n_dst = sp.n_dst;
+  const int P = layout->page_size;
+  // append plan: the new rows landing on a partial last surviving page go with
+  // that page's copy; the rest are listed per sequence for the append blocks
+  const bool app = h_new_len != nullptr;
+  std::vector<int32_t> app_tok_begin(batch + 1, 0), app_start(batch, 0), app_knew(batch, 0);
+  int64_t app_total = 0;
+  if (app) {
+    if (layer < 0 || layer >= layout->num_layers)
+      return fail(SA_ERR_SHAPE, "layer %d outside [0, %d)", layer, layout->num_layers);
+    int64_t knew = 0;
+    size_t unit_end = 0;
+    for (int b = 0; b < batch; ++b) {
+      const int n = h_new_len[b];
+      const int64_t pages_b = dst_indptr[b + 1] - dst_indptr[b];
+      if (n < 0 || dst_len[b] + (int64_t)n > pages_b * P)
+        return fail(SA_ERR_SHAPE, "sequence %d: %d new tokens after %d kept do not fit its %lld pages", b, n,
+                    dst_len[b], (long long)pages_b);
+      while (unit_end < unit_list.size() && unit_list[unit_end].seq == b) ++unit_end;
+      int first = 0;                                      // new tokens on the last surviving page
+      if (n > 0 && dst_len[b] % P != 0 && unit_end > 0 && unit_list[unit_end - 1].seq == b) {
+        sa::AsmUnit& last = unit_list[unit_end - 1];
+        last.app_row0 = dst_len[b] % P;
+        last.app_rows = std::min(P - last.app_row0, n);
+        last.app_tok = (int32_t)knew;
+        first = last.app_rows;
+      }
+      app_tok_begin[b] = (int32_t)app_total;
+      app_start[b] = dst_len[b] + first;
+      app_knew[b] = (int32_t)(knew + first);
+      app_total += n - first;
+      knew += n;
+      if (knew > INT32_MAX / 2) return fail(SA_ERR_SHAPE, "too many new tokens");
+    }
+    app_tok_begin[batch] = (int32_t)app_total;
+    if (knew > 0 && (!k_new || !v_new)) return fail(SA_ERR_NULL, "k_new / v_new is NULL");
+    if (!aligned16(k_new) || !aligned16(v_new)) return fail(SA_ERR_ALIGN, "new-row pointer not 16-byte aligned");
+  }
   if (!k_src || !v_src || !k_dst || !v_dst || !src.indptr || !src.indices || !d_fresh ||
       !d_dst_indptr || !d_dst_indices)
     return fail(SA_ERR_NULL, "a device pointer is NULL");
@@ -438,6 +480,9 @@ sa_status sa_kv_assemble(sa_ctx* ctx, const sa_layout* layout, const void* k_src
   PlanImage img;
   const size_t o_un = img.add(unit_list.data(), unit_list.size());
   const size_t o_ip = img.add(dst_indptr.data(), dst_indptr.size());
+  const size_t o_at = img.add(app_tok_begin.data(), app ? app_tok_begin.size() : 0);
+  const size_t o_as = img.add(app_start.data(), app ? app_start.size() : 0);
+  const size_t o_ak = img.add(app_knew.data(), app ? app_knew.size() : 0);
   uint8_t* dev = nullptr;
   s = upload_plan(ctx, kPlanAssemble, img, (hipStream_t)stream, &dev);
   if (s != SA_OK) return s;
@@ -461,12 +506,55 @@ sa_status sa_kv_assemble(sa_ctx* ctx, const sa_layout* layout, const void* k_src
   a.n_units = (int32_t)units;
   a.n_dst = (int32_t)n_dst;
   a.B = batch;
+  a.app_layer = app ? layer : -1;
+  a.Hkv = layout->num_kv_heads;
+  a.P = P;
+  if (app) {
+    a.k_new = (const uint16_t*)k_new;
+    a.v_new = (const uint16_t*)v_new;
+    a.app_tok_begin = (const int32_t*)(dev + o_at);
+    a.app_start = (const int32_t*)(dev + o_as);
+    a.app_knew = (const int32_t*)(dev + o_ak);
+    a.app_chunks = app_total * layout->num_kv_heads * 16;
+    a.app_blocks = (int32_t)((a.app_chunks + sa::kAsmThreads * sa::kAsmDepth - 1) / (sa::kAsmThreads * sa::kAsmDepth));
+  }
   const int64_t table_blocks = (std::max<int64_t>(n_dst, batch + 1) + sa::kAsmThreads - 1) / sa::kAsmThreads;
-  const int64_t gx = std::max<int64_t>(units, table_blocks);
-  hipLaunchKernelGGL(sa::assemble_kernel, dim3((unsigned)gx, (unsigned)layout->num_layers), dim3(sa::kAsmThreads),
-                     0, (hipStream_t)stream, a);
+  const int64_t gx = std::max<int64_t>(units + a.app_blocks, table_blocks);
+  if (gx > 0)
+    hipLaunchKernelGGL(sa::assemble_kernel, dim3((unsigned)gx, (unsigned)layout->num_layers),
+                       dim3(sa::kAsmThreads), 0, (hipStream_t)stream, a);
   SA_HIP(hipGetLastError());
   return SA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sa_status sa_kv_assemble(sa_ctx* ctx, const sa_layout* layout, const void* k_src,
+                         const void* v_src, void* k_dst, void* v_dst, int32_t batch,
+                         const int32_t* h_src_len, const int32_t* h_keep_indptr,
+                         const int32_t* h_keep_spans, const int32_t* h_reserve, sa_pages src,
+                         const int32_t* d_fresh, int32_t num_fresh, int32_t* d_dst_indptr,
+                         int32_t* d_dst_indices, int32_t dst_capacity, int32_t* h_dst_len,
+                         void* stream) {
+  return splice_launch(ctx, layout, k_src, v_src, k_dst, v_dst, batch, h_src_len, h_keep_indptr,
+                       h_keep_spans, h_reserve, src, d_fresh, num_fresh, d_dst_indptr, d_dst_indices,
+                       dst_capacity, h_dst_len, 0, nullptr, nullptr, nullptr, stream);
+}
+
+sa_status sa_kv_assemble_append(sa_ctx* ctx, const sa_layout* layout, const void* k_src,
+                                const void* v_src, void* k_dst, void* v_dst, int32_t batch,
+                                const int32_t* h_src_len, const int32_t* h_keep_indptr,
+                                const int32_t* h_keep_spans, const int32_t* h_reserve, sa_pages src,
+                                const int32_t* d_fresh, int32_t num_fresh, int32_t* d_dst_indptr,
+                                int32_t* d_dst_indices, int32_t dst_capacity, int32_t* h_dst_len,
+                                int32_t layer, const void* k_new, const void* v_new,
+                                const int32_t* h_new_len, void* stream) {
+  if (!h_new_len) return fail(SA_ERR_NULL, "h_new_len is NULL");
+  return splice_launch(ctx, layout, k_src, v_src, k_dst, v_dst, batch, h_src_len, h_keep_indptr,
+                       h_keep_spans, h_reserve, src, d_fresh, num_fresh, d_dst_indptr, d_dst_indices,
+                       dst_capacity, h_dst_len, layer, k_new, v_new, h_new_len, stream);
 }
 
 sa_status sa_kv_splice_alias(sa_ctx* ctx, const sa_layout* layout, int32_t batch,

@@ -139,6 +139,29 @@ def test_splice_alias_validation(lib):
     assert splice_alias(lib, L, [100], [1, 1], [[0, 7]], [10])[0] == 2           # indptr[0] != 0
 
 
+def assemble_append(lib, L, src_len, keep_indptr, spans, reserve, new_len, layer=0, k_new=FAKE):
+    a = [np.asarray(x, dtype=np.int32) for x in (src_len, keep_indptr, np.asarray(spans).reshape(-1),
+                                                  reserve, new_len)]
+    out = np.zeros(len(a[0]), dtype=np.int32)
+    return lib.sa_kv_assemble_append(None, ctypes.byref(L), FAKE, FAKE, FAKE, FAKE, len(a[0]),
+                                     a[0].ctypes.data, a[1].ctypes.data,
+                                     a[2].ctypes.data if a[2].size else None, a[3].ctypes.data,
+                                     sa._Pages(FAKE, FAKE), FAKE, 100, FAKE, FAKE, 100, out.ctypes.data,
+                                     layer, k_new, FAKE, a[4].ctypes.data, None)
+
+
+def test_assemble_append_validation(lib):
+    L = layout(page_size=16)
+    # 100 tokens on 7 pages, 7 pages kept (100 tokens), room for 12 more: 112 = 7 pages
+    assert assemble_append(lib, L, [100], [0, 1], [[0, 7]], [12], [12]) == 1   # host checks pass; no context
+    assert assemble_append(lib, L, [100], [0, 1], [[0, 7]], [12], [13]) == 2   # 113 tokens need an 8th page
+    assert assemble_append(lib, L, [100], [0, 1], [[0, 7]], [12], [-1]) == 2
+    assert assemble_append(lib, L, [100], [0, 1], [[0, 7]], [12], [4], layer=1) == 2
+    assert assemble_append(lib, L, [100], [0, 1], [[0, 7]], [12], [4], k_new=None) == 1
+    assert assemble_append(lib, L, [100], [0, 1], [[0, 7]], [12], [4], k_new=FAKE + 2) == 4
+    assert assemble_append(lib, L, [100], [0, 2], [[0, 2], [1, 7]], [12], [4]) == 5   # overlap
+
+
 def test_context_creation_without_gpu(lib):
     import torch
     if torch.cuda.is_available():
