@@ -6,10 +6,13 @@ tokens) is spliced by dropping a contiguous run of 171 pages (25%), leaving an
 8192-token prefix; a 2048-token transformed segment is appended after it and
 its causal grouped-query attention is computed over prefix + segment.
 
-One step = sa_kv_assemble_append (the splice and the segment's K/V append in
-one launch) -> sa_segment_prefill_attn, all on the current stream with inputs
-resident in HBM; --separate-append runs the splice and the append as two
-launches (sa_kv_assemble -> sa_kv_append) instead.  Every step uses one of R
+One step = splice, append of the segment's K/V, attention, all on the current
+stream with inputs resident in HBM.  --fuse picks the entry points:
+"splice" (default): sa_kv_assemble_append (splice and append in one launch)
+-> sa_segment_prefill_attn; "attn": sa_kv_assemble ->
+sa_segment_prefill_attn_append (two launches, or one for the append and the
+attention together with SA_APPEND_IN_ATTN=1); "none": sa_kv_assemble ->
+sa_kv_append -> sa_segment_prefill_attn.  Every step uses one of R
 disjoint copies of the cache (default 8 x 128 MB per pool), so the 256 MB
 Infinity Cache cannot hold the data a step reads from its previous use.
 
@@ -41,8 +44,8 @@ def parse():
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--rotate", type=int, default=8, help="disjoint cache copies cycled per step")
-    p.add_argument("--separate-append", action="store_true",
-                   help="splice and append as two launches instead of the fused one")
+    p.add_argument("--fuse", choices=("attn", "splice", "none"), default="splice",
+                   help="which launch carries the append (see the module docstring)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-stride", type=int, default=1, help="oracle sample: every n-th token")
     p.add_argument("--assemble-layers", type=int, default=32,
@@ -149,13 +152,13 @@ def main():
     lse = torch.empty((T, w.num_q_heads), dtype=torch.float32, device="cuda")
     ctx = sa.Context(0)
     stream = torch.cuda.current_stream()
-    fused = not args.separate_append
+    fuse = args.fuse
 
     def step(r, ev=None):
         c = copies[r % R]
         if ev is not None:
             ev[0].record(stream)
-        if fused:
+        if fuse == "splice":
             kept = sa.sa_kv_assemble_append(ctx, L, kp, vp, kp, vp, a.src_len, a.keep_indptr,
                                             a.keep_spans, a.reserve, c["sip"], c["sid"], c["fresh"],
                                             c["dip"], c["did"], 0, ks, vs, w.qlen)
@@ -166,11 +169,16 @@ def main():
                                      a.reserve, c["sip"], c["sid"], c["fresh"], c["dip"], c["did"])
             if ev is not None:
                 ev[1].record(stream)
-            sa.sa_kv_append(ctx, L, 0, kp, vp, ks, vs, kept, w.qlen, c["dip"], c["did"])
+            if fuse == "none":
+                sa.sa_kv_append(ctx, L, 0, kp, vp, ks, vs, kept, w.qlen, c["dip"], c["did"])
         if ev is not None:
             ev[2].record(stream)
-        sa.sa_segment_prefill_attn(ctx, L, 0, q, kp, vp, w.qlen, kept + w.qlen, c["dip"], c["did"],
-                                   w.scale, o, lse)
+        if fuse == "attn":
+            sa.sa_segment_prefill_attn_append(ctx, L, 0, q, kp, vp, ks, vs, w.qlen, kept + w.qlen, c["dip"],
+                                              c["did"], w.scale, o, lse)
+        else:
+            sa.sa_segment_prefill_attn(ctx, L, 0, q, kp, vp, w.qlen, kept + w.qlen, c["dip"], c["did"],
+                                       w.scale, o, lse)
         if ev is not None:
             ev[3].record(stream)
         return kept
@@ -239,10 +247,20 @@ def main():
                          "H100 80GB (SGLang, Qwen3-8B); no kernel-level numbers",
     }
 
-    if fused:
+    in_attn = fuse == "attn" and os.environ.get("SA_APPEND_IN_ATTN") == "1"
+    rec["config"]["launches"] = {"attn": "splice | append + attention" if in_attn else
+                                 "splice | append | attention (sa_segment_prefill_attn_append)",
+                                 "splice": "splice + append | attention",
+                                 "none": "splice | append | attention"}[fuse]
+    if fuse == "splice":
         sp_ms, sp_bytes = asm_ms + app_ms, asm_bytes + app_bytes
         rec["splice_append"] = {"ms": sp_ms, "bytes": sp_bytes, "gbs": sp_bytes / (sp_ms * 1e-3) / 1e9,
                                 "frac_of_hbm": sp_bytes / (sp_ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
+    elif fuse == "attn":
+        rec["assemble"] = {"ms": asm_ms + app_ms, "bytes": asm_bytes,
+                           "gbs": asm_bytes / ((asm_ms + app_ms) * 1e-3) / 1e9,
+                           "frac_of_hbm": asm_bytes / ((asm_ms + app_ms) * 1e-3) / 1e9 / PEAK_HBM_GBS}
+        rec["attn"]["includes_append_bytes"] = app_bytes
     else:
         rec["assemble"] = {"ms": asm_ms, "bytes": asm_bytes, "gbs": asm_bytes / (asm_ms * 1e-3) / 1e9,
                            "frac_of_hbm": asm_bytes / (asm_ms * 1e-3) / 1e9 / PEAK_HBM_GBS}

@@ -18,6 +18,9 @@
  *                            queries over the cached prefix plus, causally,
  *                            the segment itself (Sec. 4, prefill-attention
  *                            term: segment token i sees prefix + i + 1 keys)
+ * and, fused from them, sa_kv_assemble_append (splice + append, one launch),
+ * sa_segment_prefill_attn_append (append + attention, one launch) and the
+ * copy-free splice sa_kv_splice_alias.
  *
  * Data layout (all device memory is owned by the caller):
  *   bf16 values are IEEE bfloat16 bit patterns (uint16).
@@ -243,6 +246,36 @@ sa_status sa_segment_prefill_attn(sa_ctx *ctx, const sa_layout *layout, int32_t 
                                   int32_t batch, const int32_t *h_q_len, const int32_t *h_kv_len,
                                   sa_pages pages, float softmax_scale,
                                   void *o, float *lse, void *stream);
+
+/*
+ * sa_segment_prefill_attn_append — the segment's append and its attention in
+ * one call: each sequence's h_q_len[b] new K/V rows are written to its
+ * logical positions h_kv_len[b] - h_q_len[b] .. h_kv_len[b] - 1 (as
+ * sa_kv_append with start = kv_len - q_len), then the attention is computed
+ * exactly as sa_segment_prefill_attn does over the cache that results (paper
+ * Sec. 3.2: the lookahead builds the segment's KV on the transformed prefix).
+ * k_new / v_new: bf16 [sum h_q_len][num_kv_heads][head_dim], token-major like
+ * q; the pools are written.  The pages for the new rows must already be in
+ * the table (sa_kv_assemble's reserve).  By default this is the append
+ * kernel followed by the attention kernel on `stream`.  With the environment
+ * variable SA_APPEND_IN_ATTN=1 (read once per process) and the default
+ * attention kernel, the attention launch writes the rows itself: its blocks
+ * take the rows from a counter, publish them at device scope, and each wave
+ * waits for them only before its first tile holding a new key.  That form
+ * coordinates through counters held by the context, so its calls on one
+ * context must not overlap in time (for example on two streams at once).
+ *
+ * Errors: those of sa_segment_prefill_attn; SA_ERR_NULL for NULL new rows
+ * (when any q_len > 0), SA_ERR_ALIGN for new rows not 16-byte aligned.  A
+ * missing or out-of-range page of a new row raises the device error flag
+ * (reported by sa_sync_check) and that row is not written.
+ */
+sa_status sa_segment_prefill_attn_append(sa_ctx *ctx, const sa_layout *layout, int32_t layer,
+                                         const void *q, void *k_pool, void *v_pool,
+                                         const void *k_new, const void *v_new, int32_t batch,
+                                         const int32_t *h_q_len, const int32_t *h_kv_len,
+                                         sa_pages pages, float softmax_scale, void *o, float *lse,
+                                         void *stream);
 
 #ifdef __cplusplus
 }

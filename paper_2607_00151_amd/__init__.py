@@ -15,7 +15,7 @@ import numpy as np
 __all__ = [
     "Layout", "Context", "SaError", "library_path", "load_library",
     "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append", "sa_kv_splice_alias",
-    "sa_segment_prefill_attn", "sa_sync_check",
+    "sa_segment_prefill_attn", "sa_segment_prefill_attn_append", "sa_sync_check",
     "EXPORTED_SYMBOLS",
 ]
 
@@ -25,7 +25,7 @@ _lib = None
 
 EXPORTED_SYMBOLS = ("sa_create", "sa_destroy", "sa_status_string", "sa_last_error",
                     "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
-                    "sa_kv_splice_alias", "sa_segment_prefill_attn")
+                    "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append")
 
 STATUS = {0: "SA_OK", 1: "SA_ERR_NULL", 2: "SA_ERR_SHAPE", 3: "SA_ERR_UNSUPPORTED",
           4: "SA_ERR_ALIGN", 5: "SA_ERR_RANGE", 6: "SA_ERR_NO_PAGES", 7: "SA_ERR_HIP",
@@ -79,8 +79,10 @@ def load_library():
     lib.sa_kv_splice_alias.argtypes = [P, LP, I32, P, P, P, P, _Pages, P, I32, P, P, I32, P, P]
     lib.sa_segment_prefill_attn.argtypes = [P, LP, I32, P, P, P, I32, P, P, _Pages, ctypes.c_float,
                                             P, P, P]
+    lib.sa_segment_prefill_attn_append.argtypes = [P, LP, I32, P, P, P, P, P, I32, P, P, _Pages,
+                                                   ctypes.c_float, P, P, P]
     for name in ("sa_create", "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
-                 "sa_kv_splice_alias", "sa_segment_prefill_attn"):
+                 "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -245,4 +247,18 @@ def sa_segment_prefill_attn(ctx, layout: Layout, layer: int, q, k_pool, v_pool, 
     _check(load_library().sa_segment_prefill_attn(
         _ctx_handle(ctx), ctypes.byref(layout), int(layer), _ptr(q), _ptr(k_pool), _ptr(v_pool),
         int(len(q_len)), _ptr(q_len), _ptr(kv_len), _pages(pages_indptr, pages_indices),
+        float(softmax_scale), _ptr(o), _ptr(lse), _stream(stream)))
+
+
+def sa_segment_prefill_attn_append(ctx, layout: Layout, layer: int, q, k_pool, v_pool, k_new, v_new, q_len,
+                                   kv_len, pages_indptr, pages_indices, softmax_scale: float, o, lse=None,
+                                   stream=None):
+    """Writes each sequence's q_len new K/V rows at positions kv_len - q_len .. kv_len - 1,
+    then runs sa_segment_prefill_attn over the result (one launch with the default kernel)."""
+    q_len, kv_len = _host_i32(q_len), _host_i32(kv_len)
+    if q_len.shape != kv_len.shape:
+        raise ValueError("q_len and kv_len differ in length")
+    _check(load_library().sa_segment_prefill_attn_append(
+        _ctx_handle(ctx), ctypes.byref(layout), int(layer), _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(k_new),
+        _ptr(v_new), int(len(q_len)), _ptr(q_len), _ptr(kv_len), _pages(pages_indptr, pages_indices),
         float(softmax_scale), _ptr(o), _ptr(lse), _stream(stream)))

@@ -79,6 +79,15 @@ struct AttnArgs {
   int32_t n_items;
   int32_t Hq, Hkv, G;
   float c;                  // softmax_scale * log2(e)
+  // The segment's own K/V rows, written to their pages by the same launch
+  // (attn_pipe_kernel only; app_tickets == 0: none).
+  const uint16_t* k_new;    // [sum q_len][Hkv][kHD], token-major like q
+  const uint16_t* v_new;
+  uint32_t* sync;           // three counters kSyncStride words apart: tickets taken,
+                            // tickets written, blocks finished (zero between launches)
+  int64_t app_chunks;       // sum q_len * Hkv * 16: 16-byte chunks of K (and of V)
+  int32_t app_tickets;      // 64 ceil(app_chunks / (64 kAppTicket))
+  int32_t B;                // sequences in seqs
 };
 
 // Lazy rescaling: the exponent offset only moves when a row's running max

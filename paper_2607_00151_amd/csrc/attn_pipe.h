@@ -85,6 +85,115 @@ __device__ __forceinline__ bool table_check_finish(const AttnArgs& a, TableCheck
   return !__syncthreads_or(bad);
 }
 
+// ---- the segment's append inside the attention launch
+//
+// Every lane takes tickets from a counter (kAppTicket 16-byte chunks of K and
+// as many of V each, so that few waves hold any) until none is left, writes its chunks to their pages and
+// counts each ticket written.  A wave waits for that count to reach every
+// ticket only before it loads its first tile holding a new key (with a long
+// cached prefix, long after the writes are done).  No lane waits before it has
+// seen every ticket taken, and a lane holding a ticket finishes it without
+// waiting on anything, so every wait ends whatever number of blocks the chip
+// holds at once; a wait is still bounded (kAppSpinLimit polls, then the error
+// flag).  The ticket loop holds no barrier and no cross-lane operation, so it
+// stays correct however the compiler splits its lanes; the compiler merges
+// the lanes' counter updates into one atomic per wave.  The last block to
+// finish zeroes the counters for the next launch.  Ordering: each wave
+// releases its page writes at device scope before it counts them, and a
+// waiting wave acquires at device scope once it sees the full count, so its
+// tile loads read the new rows whichever XCD's L2 wrote them.
+constexpr int kAppTicket = 16;               // chunks of K (and of V) per ticket, a multiple of 4
+constexpr int kSyncStride = 64;              // counters 256 bytes apart
+constexpr int kAppSpinLimit = 1 << 20;       // polls of at least ~0.3 us each
+
+// Largest b with seqs[b].q_start <= t (q_start is non-decreasing).
+__device__ __forceinline__ int seq_of_token(const SeqDesc* seqs, int B, int t) {
+  int lo = 0, hi = B - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (seqs[mid].q_start <= t) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+template <int P>
+__device__ __forceinline__ void app_produce(const AttnArgs& a) {
+  const int per_tok = a.Hkv * 16;
+  uint16_t* const kp = const_cast<uint16_t*>(a.k);
+  uint16_t* const vp = const_cast<uint16_t*>(a.v);
+  for (;;) {
+    const uint32_t tk = __hip_atomic_fetch_add(a.sync, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (tk >= (uint32_t)a.app_tickets) break;
+    // ticket tk: chunks ((tk / 64) kAppTicket + j) 64 + tk % 64, so the lanes
+    // of a wave, which draw consecutive tickets, read and write consecutive chunks
+    const int64_t c0 = (int64_t)(tk >> 6) * kAppTicket * 64 + (tk & 63);
+#pragma unroll
+    for (int r = 0; r < kAppTicket; r += 4) {
+      int64_t src[4], dst[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int64_t c = c0 + (int64_t)(r + j) * 64;
+        src[j] = -1;
+        if (c >= a.app_chunks) continue;
+        const int t = (int)(c / per_tok);
+        const int rem = (int)(c - (int64_t)t * per_tok);
+        const int g = rem >> 4, ch = rem & 15;
+        const int b = seq_of_token(a.seqs, a.B, t);
+        const SeqDesc sd = a.seqs[b];
+        const int x = sd.kv_len - sd.q_len + (t - sd.q_start);
+        const int page = x / P, row = x - page * P;
+        const int32_t base = a.indptr[b];
+        if (page >= a.indptr[b + 1] - base) { atomicOr(a.err, 2); continue; }
+        const int32_t slot = a.indices[base + page];
+        if (slot < 0 || slot >= a.num_slots) { atomicOr(a.err, 2); continue; }
+        src[j] = ((int64_t)t * a.Hkv + g) * kHD + ch * 8;
+        dst[j] = (((int64_t)slot * a.Hkv + g) * P + row) * kHD + ch * 8;
+      }
+      u32x4 kx[4], vx[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (src[j] >= 0) {
+          kx[j] = ld_u32x4(a.k_new + src[j]);
+          vx[j] = ld_u32x4(a.v_new + src[j]);
+        }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (src[j] >= 0) {
+          st_u32x4(kp + dst[j], kx[j]);
+          st_u32x4(vp + dst[j], vx[j]);
+        }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __hip_atomic_fetch_add(a.sync + kSyncStride, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// One wave: returns once every ticket is written (or the poll bound is hit).
+// Every lane polls, so no region of one lane sits in the caller's loop.
+__device__ __forceinline__ void app_wait(const AttnArgs& a) {
+  for (int n = 0;; ++n) {
+    const uint32_t done = __hip_atomic_load(a.sync + kSyncStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (done >= (uint32_t)a.app_tickets) break;
+    if (n == kAppSpinLimit) {
+      atomicOr(a.err, 8);
+      break;
+    }
+    __builtin_amdgcn_s_sleep(8);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+}
+
+// Every thread of the block calls this once, at its end.
+__device__ __forceinline__ void app_finish(const AttnArgs& a) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t n = __hip_atomic_fetch_add(a.sync + 2 * kSyncStride, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (n + 1 == gridDim.x)
+#pragma unroll
+      for (int k = 0; k < 3; ++k) __hip_atomic_store(a.sync + k * kSyncStride, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
 // One group of four waves runs the item's rows over the keys
 // [g_lo, g_hi): the whole item when kGroups == 1; with two groups, group 0
 // takes the first half of the item's key tiles and group 1 the rest, and the
@@ -96,7 +205,7 @@ __device__ __forceinline__ bool table_check_finish(const AttnArgs& a, TableCheck
 // kPoolRsrc: a layer's K (and V) pool spans < 2^31 bytes, so one buffer
 // resource per pool reaches every page through the 32-bit scalar offset;
 // otherwise each page load builds a resource for its page.
-template <int P, bool kPoolRsrc, int kGroups, int GRP>
+template <int P, bool kPoolRsrc, int kGroups, int GRP, bool kApp = false>
 __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs& a, const AttnItem& it,
                                                                  const SeqDesc& sd, const PipeLds& L) {
   static_assert(P == 16 || P == 32, "page size");
@@ -439,6 +548,19 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
   lds_u8* const V0 = L.v0;
   lds_u8* const V1 = L.v1;
 
+  // Tiles from t_seg on hold keys this launch appends: the step that issues
+  // the first such load waits for the append (step t loads tiles t + 1 and
+  // t + 2; the prologue loads t0 and t0 + 1).
+  int t_wait = -1;
+  if constexpr (kApp) {
+    static_assert(kGroups == 1, "the append runs with one group per block");
+    const int t_seg = pre / kKT;
+    if (t_seg < t1) {
+      if (t_seg <= t0 + 1) app_wait(a);
+      else t_wait = t_seg - 2;
+    }
+  }
+
   // ---- prologue: K(t0), V(t0), K(t0 + 1); S(t0) and its rescale test
   if (t0 < t1) {
     const Slots s0 = fetch(t0);
@@ -513,16 +635,19 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
   const int t_fast = (wave_active && table_ok) ? max(t0, min(w_full / kKT - 1, t1 - 2)) : t0;
   int t = t0;
   for (; t + 1 < t_fast; t += 2) {
+    if (kApp && t == t_wait) app_wait(a);
     priority(t);
     wait_tiles();
     advance_fast(t);
     fast_step(IntC<0>{}, K1, V0, K0, V1);
+    if (kApp && t + 1 == t_wait) app_wait(a);
     priority(t + 1);
     wait_tiles();
     advance_fast(t + 1);
     fast_step(IntC<1>{}, K0, V1, K1, V0);
   }
   if (t < t_fast) {
+    if (kApp && t == t_wait) app_wait(a);
     priority(t);
     wait_tiles();
     advance_fast(t);
@@ -538,6 +663,7 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
   }
   for (; t < t1; ++t) {
     const bool odd = (t - t0) & 1;
+    if (kApp && t == t_wait) app_wait(a);
     priority(t);
     top(t, odd ? K1 : K0, odd ? V0 : V1);
     plain_step(t, odd ? K0 : K1, odd ? V1 : V0);
@@ -634,16 +760,20 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
 }
 
 // One group of four waves per block, two blocks per CU.
-template <int P, bool kPoolRsrc>
+// kApp: the launch also writes the segment's new K/V rows (app_produce).
+template <int P, bool kPoolRsrc, bool kApp>
 __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t k_lds0[kTileBytes], k_lds1[kTileBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t v_lds0[kTileBytes], v_lds1[kTileBytes];
+  if constexpr (kApp) app_produce<P>(a);
   const AttnItem it = ld_uniform(a.items + blockIdx.x);
-  if (it.kv_begin >= it.kv_end) return;                     // padding item
-  const SeqDesc sd{it.q_start, it.q_len, it.kv_len, 0};
-  const PipeLds L{(lds_u8*)k_lds0, (lds_u8*)k_lds1, (lds_u8*)v_lds0, (lds_u8*)v_lds1,
-                  nullptr, nullptr, nullptr, nullptr, nullptr};
-  pipe_group<P, kPoolRsrc, 1, 0>(a, it, sd, L);
+  if (it.kv_begin < it.kv_end) {                            // else a padding item
+    const SeqDesc sd{it.q_start, it.q_len, it.kv_len, 0};
+    const PipeLds L{(lds_u8*)k_lds0, (lds_u8*)k_lds1, (lds_u8*)v_lds0, (lds_u8*)v_lds1,
+                    nullptr, nullptr, nullptr, nullptr, nullptr};
+    pipe_group<P, kPoolRsrc, 1, 0, kApp>(a, it, sd, L);
+  }
+  if constexpr (kApp) app_finish(a);
 }
 
 // Two groups of four waves per block on the same rows, each over half of the

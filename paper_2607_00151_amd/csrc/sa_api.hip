@@ -81,6 +81,7 @@ struct sa_ctx {
   int ring_next = 0;
   float* part = nullptr;           // split-KV partials
   size_t part_cap = 0;             // bytes
+  uint32_t* d_sync = nullptr;      // counters of an attention launch that appends (zero between launches)
 };
 
 namespace {
@@ -176,16 +177,33 @@ AttnVariant attn_variant() {
   return kVariants[v];
 }
 
+// sa_segment_prefill_attn_append writes the segment's rows with the append
+// kernel and then runs the attention (two launches) unless
+// SA_APPEND_IN_ATTN=1, which has the default attention kernel write them
+// itself in the same launch (measured slower at the c2 workload: the
+// cross-block publication of the rows costs more than the launch it saves).
+bool append_in_attention() {
+  static bool v = [] {
+    const char* e = getenv("SA_APPEND_IN_ATTN");
+    return e != nullptr && atoi(e) == 1;
+  }();
+  return v;
+}
+
 template <int P>
 void launch_attn_p(AttnVariant v, bool pool_rsrc, dim3 grid, hipStream_t st, const sa::AttnArgs& a) {
   if (v.pipe == 2 && pool_rsrc)
     hipLaunchKernelGGL((sa::attn_pp_kernel<P, true>), grid, dim3(512), 0, st, a);
   else if (v.pipe == 2)
     hipLaunchKernelGGL((sa::attn_pp_kernel<P, false>), grid, dim3(512), 0, st, a);
+  else if (v.pipe && a.app_tickets > 0 && pool_rsrc)
+    hipLaunchKernelGGL((sa::attn_pipe_kernel<P, true, true>), grid, dim3(256), 0, st, a);
+  else if (v.pipe && a.app_tickets > 0)
+    hipLaunchKernelGGL((sa::attn_pipe_kernel<P, false, true>), grid, dim3(256), 0, st, a);
   else if (v.pipe && pool_rsrc)
-    hipLaunchKernelGGL((sa::attn_pipe_kernel<P, true>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((sa::attn_pipe_kernel<P, true, false>), grid, dim3(256), 0, st, a);
   else if (v.pipe)
-    hipLaunchKernelGGL((sa::attn_pipe_kernel<P, false>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((sa::attn_pipe_kernel<P, false, false>), grid, dim3(256), 0, st, a);
   else
     hipLaunchKernelGGL((sa::attn_kernel<P, 1, 4>), grid, dim3(256), 0, st, a);
 }
@@ -234,6 +252,10 @@ sa_status sa_create(int device, sa_ctx** out) {
   c->num_cu = prop.multiProcessorCount;
   hipError_t e = hipMalloc(&c->d_err, sizeof(int32_t));
   if (e == hipSuccess) e = hipMemset(c->d_err, 0, sizeof(int32_t));
+  const size_t sync_bytes = 3 * sa::kSyncStride * sizeof(uint32_t);
+  if (e == hipSuccess) e = hipMalloc(&c->d_sync, sync_bytes);
+  if (e == hipSuccess) e = hipMemset(c->d_sync, 0, sync_bytes);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
   for (int i = 0; e == hipSuccess && i < kRing; ++i)
     e = hipEventCreateWithFlags(&c->ring[i].ev, hipEventDisableTiming);
   if (e != hipSuccess) {
@@ -255,6 +277,7 @@ void sa_destroy(sa_ctx* ctx) {
     if (s.ev) (void)hipEventDestroy(s.ev);
   }
   if (ctx->part) (void)hipFree(ctx->part);
+  if (ctx->d_sync) (void)hipFree(ctx->d_sync);
   if (ctx->d_err) (void)hipFree(ctx->d_err);
   delete ctx;
 }
@@ -602,11 +625,18 @@ sa_status sa_kv_splice_alias(sa_ctx* ctx, const sa_layout* layout, int32_t batch
 
 // ---------------------------------------------------------------- attention
 
-sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t layer,
-                                  const void* q, const void* k_pool, const void* v_pool,
-                                  int32_t batch, const int32_t* h_q_len, const int32_t* h_kv_len,
-                                  sa_pages pages, float softmax_scale, void* o, float* lse,
-                                  void* stream) {
+}  // extern "C"
+
+namespace {
+
+// The attention launch; with `append` it first writes each sequence's q_len
+// new K/V rows (k_new, v_new) to its positions kv_len - q_len .. kv_len - 1:
+// as an append launch before the attention, or inside the attention launch
+// (append_in_attention()).
+sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const void* q,
+                      const void* k_pool, const void* v_pool, bool append, const void* k_new,
+                      const void* v_new, int32_t batch, const int32_t* h_q_len, const int32_t* h_kv_len,
+                      sa_pages pages, float softmax_scale, void* o, float* lse, void* stream) {
   sa_status s = check_layout(layout);
   if (s != SA_OK) return s;
   if (layer < 0 || layer >= layout->num_layers)
@@ -634,12 +664,24 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
   if (!aligned16(q) || !aligned16(o) || !aligned16(k_pool) || !aligned16(v_pool) ||
       (reinterpret_cast<uintptr_t>(lse) & 3u))
     return fail(SA_ERR_ALIGN, "q, o, pools must be 16-byte aligned (lse 4-byte)");
+  if (append && total_q > 0 && (!k_new || !v_new)) return fail(SA_ERR_NULL, "k_new / v_new is NULL");
+  if (append && (!aligned16(k_new) || !aligned16(v_new)))
+    return fail(SA_ERR_ALIGN, "new-row pointer not 16-byte aligned");
   s = check_ctx(ctx);
   if (s != SA_OK) return s;
   if (total_q == 0) return SA_OK;
 
   // ---- kernel variant: query rows per wave (32 * qt) and waves per work item
   const AttnVariant var = attn_variant();
+  const bool fused = append && var.pipe == 1 && append_in_attention();
+  if (append && !fused) {
+    // the new rows go in with an append launch of their own
+    std::vector<int32_t> start(batch);
+    for (int b = 0; b < batch; ++b) start[b] = h_kv_len[b] - h_q_len[b];
+    s = sa_kv_append(ctx, layout, layer, const_cast<void*>(k_pool), const_cast<void*>(v_pool), k_new, v_new,
+                     batch, start.data(), h_q_len, pages, stream);
+    if (s != SA_OK) return s;
+  }
   const int rows_item = 32 * var.qt * var.waves;
 
   // ---- work items: (sequence, kv head, row tile), longest first
@@ -795,6 +837,17 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
   a.Hkv = Hkv;
   a.G = G;
   a.c = softmax_scale * 1.4426950408889634f;
+  a.B = batch;
+  if (fused) {
+    a.k_new = (const uint16_t*)k_new;
+    a.v_new = (const uint16_t*)v_new;
+    a.sync = ctx->d_sync;
+    a.app_chunks = total_q * Hkv * 16;
+    // whole groups of 64 tickets (one wave's draw) cover the chunks
+    const int64_t tickets = (a.app_chunks + 64 * sa::kAppTicket - 1) / (64 * sa::kAppTicket) * 64;
+    if (tickets > INT32_MAX / 2) return fail(SA_ERR_SHAPE, "too many new rows for one launch");
+    a.app_tickets = (int32_t)tickets;
+  }
   const bool pool_rsrc = layer_elems(layout) * 2 < ((int64_t)1 << 31);
   launch_attn(layout->page_size, var, pool_rsrc, dim3((unsigned)items.size()), (hipStream_t)stream, a);
   SA_HIP(hipGetLastError());
@@ -814,6 +867,28 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
     SA_HIP(hipGetLastError());
   }
   return SA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t layer,
+                                  const void* q, const void* k_pool, const void* v_pool,
+                                  int32_t batch, const int32_t* h_q_len, const int32_t* h_kv_len,
+                                  sa_pages pages, float softmax_scale, void* o, float* lse,
+                                  void* stream) {
+  return attn_launch(ctx, layout, layer, q, k_pool, v_pool, false, nullptr, nullptr, batch, h_q_len,
+                     h_kv_len, pages, softmax_scale, o, lse, stream);
+}
+
+sa_status sa_segment_prefill_attn_append(sa_ctx* ctx, const sa_layout* layout, int32_t layer,
+                                         const void* q, void* k_pool, void* v_pool, const void* k_new,
+                                         const void* v_new, int32_t batch, const int32_t* h_q_len,
+                                         const int32_t* h_kv_len, sa_pages pages, float softmax_scale,
+                                         void* o, float* lse, void* stream) {
+  return attn_launch(ctx, layout, layer, q, k_pool, v_pool, true, k_new, v_new, batch, h_q_len,
+                     h_kv_len, pages, softmax_scale, o, lse, stream);
 }
 
 }  // extern "C"

@@ -74,6 +74,26 @@ def test_attn_validation(lib):
     assert b"context" in lib.sa_last_error()
 
 
+def attn_append(lib, L, q_len, kv_len, k_new=FAKE, v_new=FAKE, layer=0):
+    ql = np.asarray(q_len, dtype=np.int32)
+    kl = np.asarray(kv_len, dtype=np.int32)
+    return lib.sa_segment_prefill_attn_append(None, ctypes.byref(L), layer, FAKE, FAKE, FAKE, k_new, v_new,
+                                              len(ql), ql.ctypes.data, kl.ctypes.data,
+                                              sa._Pages(FAKE, FAKE), 0.1, FAKE, None, None)
+
+
+def test_attn_append_validation(lib):
+    assert attn_append(lib, layout(), [4], [8]) == 1                # all valid -> NULL ctx
+    assert b"context" in lib.sa_last_error()
+    assert attn_append(lib, layout(), [4], [8], k_new=None) == 1
+    assert b"k_new" in lib.sa_last_error()
+    assert attn_append(lib, layout(), [4], [8], v_new=FAKE + 4) == 4
+    assert attn_append(lib, layout(), [9], [8]) == 2
+    assert attn_append(lib, layout(), [4], [8], layer=1) == 2
+    assert attn_append(lib, layout(), [0], [8], k_new=None, v_new=None) == 1   # no new rows: still needs ctx
+    assert b"context" in lib.sa_last_error()
+
+
 def append(lib, L, start, new_len, k_new=FAKE, layer=0):
     st = np.asarray(start, dtype=np.int32)
     nl = np.asarray(new_len, dtype=np.int32)

@@ -157,6 +157,67 @@ def test_split_kv_and_merge(ctx):
     check_lse(w, lse.cpu().numpy(), ref_lse)
 
 
+def check_attention_append(ctx, w, launches=2):
+    """sa_segment_prefill_attn_append over a cache holding only the prefix (layer 1 of
+    two): both pools end exactly as the oracle's append leaves them, and every output
+    row and LSE matches the oracle.  Each launch starts from fresh pools, so the second
+    also shows the launch left its counters ready for the next."""
+    L = layout_of(w, num_layers=2)
+    layer = 1
+    ip, ix = dev_i32(w.pages_indptr), dev_i32(w.pages)
+    ref, ref_lse, _ = oracle_all(w)
+    sl, ro = opages.append_destinations(w.pre, w.qlen, w.pages_indptr, w.pages, w.page_size)
+    T = int(w.q_indptr[-1])
+    for n in range(launches):
+        kp, vp = new_pool(w, 2), new_pool(w, 2)
+        for pool, full in ((kp, w.k), (vp, w.v)):
+            place_range(pool, layer, w, lambda b, full=full: full[w.prefix_rows(b)], w.pages_indptr,
+                        w.pages, w.pre)
+        want = [host_u16(kp), host_u16(vp)]
+        o = torch.empty((T, w.num_q_heads, 128), dtype=torch.int16, device="cuda")
+        lse = torch.empty((T, w.num_q_heads), dtype=torch.float32, device="cuda")
+        sa.sa_segment_prefill_attn_append(ctx, L, layer, dev_u16(w.q), kp, vp, dev_u16(w.k_seg()),
+                                          dev_u16(w.v_seg()), w.qlen, w.kv, ip, ix, w.scale, o, lse)
+        sa.sa_sync_check(ctx)
+        for wa, new, got in ((want[0], w.k_seg(), kp), (want[1], w.v_seg(), vp)):
+            opages.apply_append(wa[layer], new, sl, ro)
+            assert np.array_equal(host_u16(got), wa), n
+        mx, mean = compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
+        check_lse(w, lse.cpu().numpy(), ref_lse)
+    print(f"  {w.name}: max {mx:.3e} mean {mean:.3e}", flush=True)
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_append_inside_attention_all_rows(ctx, name):
+    print(f"attention with append {name}", flush=True)
+    check_attention_append(ctx, small(name))
+
+
+def test_append_inside_attention_split_kv(ctx):
+    """Key-range split items: some end before the new keys, some start inside them."""
+    print("attention with append, split", flush=True)
+    check_attention_append(ctx, build("split", 21, 8, 1, 128, 16, [5000, 3000, 70, 0], [1, 1, 3, 1]))
+
+
+def test_append_inside_attention_missing_page_is_reported(ctx):
+    """A new row whose page is not in the table is skipped and reported."""
+    print("attention with append, missing page", flush=True)
+    w = build("short", 51, 8, 2, 128, 16, [20], [40])
+    L = layout_of(w)
+    ip = dev_i32([0, 2])                          # 60 tokens need 4 pages; the table has 2
+    ix = dev_i32(w.pages[:2])
+    T = int(w.qlen.sum())
+    kp, vp = new_pool(w), new_pool(w)
+    o = torch.empty((T, w.num_q_heads, 128), dtype=torch.int16, device="cuda")
+    sa.sa_segment_prefill_attn_append(ctx, L, 0, dev_u16(w.q), kp, vp, dev_u16(w.k_seg()), dev_u16(w.v_seg()),
+                                      w.qlen, w.kv, ip, ix, w.scale, o)
+    with pytest.raises(sa.SaError) as e:
+        sa.sa_sync_check(ctx)
+    assert e.value.name == "SA_ERR_RANGE"
+    sa.sa_sync_check(ctx)
+    check_attention_append(ctx, workloads.make("c1"), launches=1)   # the next launch is whole
+
+
 def test_page_permutation_invariance(ctx):
     """Where the pages sit in the pool does not change a single output bit."""
     w = workloads.make("c1")
@@ -229,11 +290,24 @@ def test_out_of_range_slot_is_reported(ctx):
 
 # ------------------------------------------------------ whole step, full size
 
-def run_step(ctx, w, L, state, alias=False):
-    """assemble (commit splice; zero-copy with alias) -> append (segment) -> attention, as
-    timed by the bench."""
+def run_step(ctx, w, L, state, mode="copy"):
+    """assemble (commit splice; zero-copy in mode "alias") -> append (segment) -> attention;
+    mode "splice_append" runs the first two as one launch (as the bench does), mode
+    "attn_append" the last two."""
     kp, vp, sip, sid, fresh, dip, did, q, ks, vs, o, lse = state
     a = w.asm
+    if mode == "splice_append":
+        dst_len = sa.sa_kv_assemble_append(ctx, L, kp, vp, kp, vp, a.src_len, a.keep_indptr, a.keep_spans,
+                                           a.reserve, sip, sid, fresh, dip, did, 0, ks, vs, w.qlen)
+        sa.sa_segment_prefill_attn(ctx, L, 0, q, kp, vp, w.qlen, dst_len + w.qlen, dip, did, w.scale, o, lse)
+        return dst_len
+    if mode == "attn_append":
+        dst_len = sa.sa_kv_assemble(ctx, L, kp, vp, kp, vp, a.src_len, a.keep_indptr, a.keep_spans,
+                                    a.reserve, sip, sid, fresh, dip, did)
+        sa.sa_segment_prefill_attn_append(ctx, L, 0, q, kp, vp, ks, vs, w.qlen, dst_len + w.qlen, dip, did,
+                                          w.scale, o, lse)
+        return dst_len
+    alias = mode == "alias"
     if alias:
         dst_len = sa.sa_kv_splice_alias(ctx, L, a.src_len, a.keep_indptr, a.keep_spans, a.reserve, sip,
                                         sid, fresh, dip, did)
@@ -246,7 +320,8 @@ def run_step(ctx, w, L, state, alias=False):
     return dst_len
 
 
-def check_step(ctx, w, per_seq_rows, alias=False):
+def check_step(ctx, w, per_seq_rows, mode="copy"):
+    alias = mode == "alias"
     L = layout_of(w)
     kp, vp, sip, sid, fresh = build_source_cache(w)
     if alias:
@@ -260,7 +335,7 @@ def check_step(ctx, w, per_seq_rows, alias=False):
     lse = torch.empty((T, w.num_q_heads), dtype=torch.float32, device="cuda")
     state = (kp, vp, sip, sid, fresh, dip, did, dev_u16(w.q), dev_u16(w.k_seg()),
              dev_u16(w.v_seg()), o, lse)
-    dst_len = run_step(ctx, w, L, state, alias)
+    dst_len = run_step(ctx, w, L, state, mode)
     sa.sa_sync_check(ctx)
     assert np.array_equal(dst_len, w.pre)
     # the assembled cache reads back as prefix ++ segment, bit for bit (sampled sequences)
@@ -304,7 +379,14 @@ def test_step_small(ctx, name):
 
 @pytest.mark.parametrize("name", WITH_ASM)
 def test_step_small_zero_copy_splice(ctx, name):
-    check_step(ctx, small(name), per_seq_rows=64, alias=True)
+    check_step(ctx, small(name), per_seq_rows=64, mode="alias")
+
+
+@pytest.mark.parametrize("mode", ["splice_append", "attn_append"])
+@pytest.mark.parametrize("name", WITH_ASM)
+def test_step_small_fused(ctx, name, mode):
+    print(f"step {mode} {name}", flush=True)
+    check_step(ctx, small(name), per_seq_rows=64, mode=mode)
 
 
 @pytest.mark.parametrize("name", WITH_ASM)
@@ -351,18 +433,32 @@ def test_step_c2_full(ctx):
     check_step(ctx, workloads.make("c2"), per_seq_rows=512)
 
 
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("mode", ["splice_append", "attn_append"])
+def test_step_c2_full_fused(ctx, mode):
+    print(f"c2 full step, {mode}", flush=True)
+    check_step(ctx, workloads.make("c2"), per_seq_rows=256, mode=mode)
+
+
 @pytest.mark.timeout(900)
 def test_step_c3_full(ctx):
     print("c3 full step", flush=True)
     check_step(ctx, workloads.make("c3"), per_seq_rows=48)
 
 
-def check_direct(ctx, w, per_seq_rows, extra_rows=None):
+def check_direct(ctx, w, per_seq_rows, extra_rows=None, fused=False):
     L = layout_of(w)
     kp, vp, ip, ix = build_cache(w, with_segment=False)
-    sa.sa_kv_append(ctx, L, 0, kp, vp, dev_u16(w.k_seg()), dev_u16(w.v_seg()), w.pre, w.qlen,
-                    ip, ix)
-    o, lse = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    if fused:
+        T = int(w.qlen.sum())
+        o = torch.empty((T, w.num_q_heads, 128), dtype=torch.int16, device="cuda")
+        lse = torch.empty((T, w.num_q_heads), dtype=torch.float32, device="cuda")
+        sa.sa_segment_prefill_attn_append(ctx, L, 0, dev_u16(w.q), kp, vp, dev_u16(w.k_seg()),
+                                          dev_u16(w.v_seg()), w.qlen, w.kv, ip, ix, w.scale, o, lse)
+    else:
+        sa.sa_kv_append(ctx, L, 0, kp, vp, dev_u16(w.k_seg()), dev_u16(w.v_seg()), w.pre, w.qlen,
+                        ip, ix)
+        o, lse = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
     sa.sa_sync_check(ctx)
     toks, heads = sample_rows(w, per_seq_rows)
     if extra_rows is not None:
@@ -395,6 +491,7 @@ def test_c4_full_outliers(ctx):
 
 
 @pytest.mark.timeout(600)
-def test_c5_full_mixed(ctx):
-    print("c5 full", flush=True)
-    check_direct(ctx, workloads.make("c5"), per_seq_rows=24)
+@pytest.mark.parametrize("fused", [False, True])
+def test_c5_full_mixed(ctx, fused):
+    print(f"c5 full, append inside attention {fused}", flush=True)
+    check_direct(ctx, workloads.make("c5"), per_seq_rows=24, fused=fused)
