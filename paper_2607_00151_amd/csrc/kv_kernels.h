@@ -40,12 +40,17 @@ __device__ __forceinline__ int find_seq(const int32_t* tok_begin, int B, int t) 
 
 constexpr int kAppendChunksPerThread = 4;
 
+// Each thread resolves the slots of its chunks first, then issues every load,
+// then every store: the stores may alias the new rows as far as the compiler
+// knows, so a load placed after a store would wait for it.
 __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
   const int per_tok = a.Hkv * 16;
+  int64_t dst[kAppendChunksPerThread];
 #pragma unroll
   for (int u = 0; u < kAppendChunksPerThread; ++u) {
     const int64_t c = ((int64_t)blockIdx.x * kAppendChunksPerThread + u) * 256 + threadIdx.x;
-    if (c >= a.total_chunks) return;
+    dst[u] = -1;
+    if (c >= a.total_chunks) continue;
     const int t = (int)(c / per_tok);
     const int rem = (int)(c - (int64_t)t * per_tok);
     const int g = rem >> 4, ch = rem & 15;
@@ -56,12 +61,22 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
     if (page >= a.indptr[b + 1] - base) { atomicOr(a.err, 2); continue; }
     const int32_t slot = a.indices[base + page];
     if (slot < 0 || (int64_t)slot >= a.num_slots) { atomicOr(a.err, 2); continue; }
-    const int64_t dst = (((int64_t)slot * a.Hkv + g) * a.P + row) * 128 + ch * 8;
-    const u32x4 kx = ld_u32x4(a.k_new + c * 8);
-    const u32x4 vx = ld_u32x4(a.v_new + c * 8);
-    st_u32x4(a.k_pool + dst, kx);
-    st_u32x4(a.v_pool + dst, vx);
+    dst[u] = (((int64_t)slot * a.Hkv + g) * a.P + row) * 128 + ch * 8;
   }
+  u32x4 kx[kAppendChunksPerThread], vx[kAppendChunksPerThread];
+#pragma unroll
+  for (int u = 0; u < kAppendChunksPerThread; ++u)
+    if (dst[u] >= 0) {
+      const int64_t c = ((int64_t)blockIdx.x * kAppendChunksPerThread + u) * 256 + threadIdx.x;
+      kx[u] = ld_u32x4(a.k_new + c * 8);
+      vx[u] = ld_u32x4(a.v_new + c * 8);
+    }
+#pragma unroll
+  for (int u = 0; u < kAppendChunksPerThread; ++u)
+    if (dst[u] >= 0) {
+      st_u32x4(a.k_pool + dst[u], kx[u]);
+      st_u32x4(a.v_pool + dst[u], vx[u]);
+    }
 }
 
 // ---------------------------------------------------------------- assemble
