@@ -52,6 +52,9 @@ def parse():
     p.add_argument("--cpu-stride", type=int, default=1, help="oracle sample: every n-th token")
     p.add_argument("--assemble-layers", type=int, default=32,
                    help="layers of the separate all-layer assemble measurement (0: skip)")
+    p.add_argument("--config", choices=("c1", "c2", "c3", "c4", "c5"), default="c2",
+                   help="workload; c2 is the benchmark line, the others are measured the same way "
+                        "(splice where the configuration has one, append, attention) without rotation")
     p.add_argument("--copy-bytes", type=int, default=0,
                    help="instead of the step, time a plain device copy of this many bytes "
                         "(calibrates the FETCH_SIZE / WRITE_SIZE counters)")
@@ -105,6 +108,121 @@ def copy_mode(nbytes: int, steps: int, warmup: int):
                       "ms": ms, "gbs": 4 * n / (ms * 1e-3) / 1e9}), flush=True)
 
 
+def config_mode(args):
+    """One configuration other than the benchmark line: each step is the splice with
+    the append (configurations with an assembly step) or the append alone, then the
+    attention, on one cache (these caches exceed the 256 MB Infinity Cache, c1 aside)."""
+    import torch
+    import paper_2607_00151_amd as sa
+    if not os.path.exists(sa.library_path()):
+        from paper_2607_00151_amd import build
+        build.build()
+    import workloads
+    from harness import build_cache, build_source_cache, dev_i32, dev_u16
+
+    w = workloads.make(args.config)
+    L = sa.Layout(num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads, head_dim=128,
+                  page_size=w.page_size, num_layers=1, num_slots=w.num_slots)
+    T = int(w.qlen.sum())
+    Hkv, P, Hq = w.num_kv_heads, w.page_size, w.num_q_heads
+    q, ks, vs = dev_u16(w.q), dev_u16(w.k_seg()), dev_u16(w.v_seg())
+    o = torch.empty((T, Hq, 128), dtype=torch.int16, device="cuda")
+    lse = torch.empty((T, Hq), dtype=torch.float32, device="cuda")
+    ctx = sa.Context(0)
+    stream = torch.cuda.current_stream()
+    app_bytes = 2 * T * Hkv * 128 * 2 * 2
+    a = w.asm
+    if a is not None:
+        kp, vp, sip, sid, fresh = build_source_cache(w)
+        dip = torch.zeros(w.batch + 1, dtype=torch.int32, device="cuda")
+        did = torch.zeros(len(a.fresh), dtype=torch.int32, device="cuda")
+        kept_pages = int(sum(e - b for b, e in a.keep_spans))
+        n_dst = int(sum(-(-int(x + y) // P) for x, y in zip(w.pre, w.qlen)))
+        first_bytes = 2 * kept_pages * 2 * Hkv * P * 128 * 2 + 4 * (n_dst + kept_pages + w.batch + 1) + app_bytes
+        first_name = "splice_append"
+
+        def first():
+            return sa.sa_kv_assemble_append(ctx, L, kp, vp, kp, vp, a.src_len, a.keep_indptr, a.keep_spans,
+                                            a.reserve, sip, sid, fresh, dip, did, 0, ks, vs, w.qlen)
+        pages = (dip, did)
+    else:
+        kp, vp, ip, ix = build_cache(w, with_segment=False)
+        first_bytes, first_name = app_bytes, "append"
+
+        def first():
+            sa.sa_kv_append(ctx, L, 0, kp, vp, ks, vs, w.pre, w.qlen, ip, ix)
+            return w.pre
+        pages = (ip, ix)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        kept = first()
+        if ev is not None:
+            ev[1].record(stream)
+        sa.sa_segment_prefill_attn(ctx, L, 0, q, kp, vp, w.qlen, kept + w.qlen, pages[0], pages[1], w.scale, o, lse)
+        if ev is not None:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    sa.sa_sync_check(ctx)
+    K = args.steps
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(K):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t0.elapsed_time(t1) / K
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    for e in evs:
+        step(e)
+    torch.cuda.synchronize()
+    sa.sa_sync_check(ctx)
+    first_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    attn_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    flops = w.attn_flops()
+    tflops = flops / (attn_ms * 1e-3) / 1e12
+    rec = {
+        "metric": "segment-prefill tokens/s + attn TFLOP/s (% MFMA peak); KV assemble GB/s (% HBM)",
+        "value": T / (ms_per_step * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
+        "ms_per_step": ms_per_step, "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{w.name}: batch {w.batch}, Hq {Hq} / Hkv {Hkv} / d 128, page {P}, "
+                               f"prefix {int(w.pre.min())}..{int(w.pre.max())}, segment {int(w.qlen.min())}.."
+                               f"{int(w.qlen.max())}", "segment_tokens": T, "cached_keys": int(w.kv.sum())},
+        "attn": {"ms": attn_ms, "gflop": flops / 1e9, "tflops": tflops, "frac_of_bf16_peak": tflops / PEAK_BF16_TFLOPS},
+        first_name: {"ms": first_ms, "bytes": first_bytes, "gbs": first_bytes / (first_ms * 1e-3) / 1e9,
+                     "frac_of_hbm": first_bytes / (first_ms * 1e-3) / 1e9 / PEAK_HBM_GBS},
+    }
+    dec = w.qlen == 1
+    if dec.any() and not dec.all():
+        # the same launch over only the decode rows, and over only the prefill segments
+        for name, sel in (("decode_only", dec), ("prefill_only", ~dec)):
+            rows = np.concatenate([np.arange(w.q_indptr[b], w.q_indptr[b + 1]) for b in np.nonzero(sel)[0]])
+            qs = dev_u16(w.q[rows])
+            os_ = torch.empty((len(rows), Hq, 128), dtype=torch.int16, device="cuda")
+            ql = np.where(sel, w.qlen, 0)
+            sub = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+            for i in range(args.warmup + K):
+                if i >= args.warmup:
+                    sub[i - args.warmup][0].record(stream)
+                sa.sa_segment_prefill_attn(ctx, L, 0, qs, kp, vp, ql, np.where(sel, w.kv, 0), pages[0], pages[1],
+                                           w.scale, os_)
+                if i >= args.warmup:
+                    sub[i - args.warmup][1].record(stream)
+            torch.cuda.synchronize()
+            sa.sa_sync_check(ctx)
+            keys = int(w.kv[sel].sum())
+            rec[name] = {"ms": float(np.mean([x.elapsed_time(y) for x, y in sub])), "rows": int(len(rows)),
+                         "cached_keys": keys}
+        d = rec["decode_only"]
+        d["kv_gbs"] = d["cached_keys"] * Hkv * 128 * 2 * 2 / (d["ms"] * 1e-3) / 1e9
+    ctx.close()
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -113,6 +231,9 @@ def main():
         sys.exit(2)
     if args.copy_bytes:
         copy_mode(args.copy_bytes, args.steps, args.warmup)
+        return
+    if args.config != "c2":
+        config_mode(args)
         return
 
     import torch
