@@ -218,6 +218,50 @@ def test_append_inside_attention_missing_page_is_reported(ctx):
     check_attention_append(ctx, workloads.make("c1"), launches=1)   # the next launch is whole
 
 
+def test_first_row_without_prefix_is_v0_bitwise(ctx):
+    """With no cached prefix, segment row 0 sees only key 0: its output is v_0 bit for bit
+    (p = 2^0 = 1 on both sides of the division), for every query head of the group."""
+    w = build("v0", 61, 8, 2, 128, 16, [0, 0, 37], [5, 70, 3])
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    o, _ = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    sa.sa_sync_check(ctx)
+    got = host_u16(o)
+    G = w.num_q_heads // w.num_kv_heads
+    for b in (0, 1):
+        t, kv0 = int(w.q_indptr[b]), int(w.kv_indptr[b])
+        for h in range(w.num_q_heads):
+            assert np.array_equal(got[t, h], w.v[kv0, h // G]), (b, h)
+
+
+def test_constant_values_and_zero_keys_closed_forms(ctx):
+    """V = c everywhere gives O = c; K = 0 gives each row the mean of the values it sees."""
+    w = build("closed", 62, 8, 2, 128, 16, [300, 0], [90, 130])
+    L = layout_of(w)
+    c = 0.375
+    w.v[:] = workloads.rng.f32_to_bf16_bits(np.full(w.v.shape, c, dtype=np.float32))
+    kp, vp, ip, ix = build_cache(w)
+    o, _ = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    sa.sa_sync_check(ctx)
+    got = (host_u16(o).astype(np.uint32) << 16).view(np.float32)
+    assert np.abs(got - c).max() <= c * 2.0 ** -8          # P rounded to bf16 in the numerator only
+
+    w = build("closed", 63, 8, 2, 128, 16, [300, 0], [90, 130])
+    w.k[:] = 0
+    kp, vp, ip, ix = build_cache(w)
+    o, _ = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    sa.sa_sync_check(ctx)
+    bits = host_u16(o)
+    vf = (w.v.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    G = w.num_q_heads // w.num_kv_heads
+    for b in range(w.batch):
+        k0, pre = int(w.kv_indptr[b]), int(w.pre[b])
+        run = np.cumsum(vf[k0: k0 + int(w.kv[b])], axis=0) / np.arange(1, int(w.kv[b]) + 1)[:, None, None]
+        for i in range(int(w.qlen[b])):
+            want = np.repeat(run[pre + i], G, axis=0)            # [Hq][D]
+            compare(bits[int(w.q_indptr[b]) + i], want, MAX_TOL, MEAN_TOL)
+
+
 def test_page_permutation_invariance(ctx):
     """Where the pages sit in the pool does not change a single output bit."""
     w = workloads.make("c1")
