@@ -491,8 +491,10 @@ sa_status splice_launch(sa_ctx* ctx, const sa_layout* layout, const void* k_src,
     if (knew > 0 && (!k_new || !v_new)) return fail(SA_ERR_NULL, "k_new / v_new is NULL");
     if (!aligned16(k_new) || !aligned16(v_new)) return fail(SA_ERR_ALIGN, "new-row pointer not 16-byte aligned");
   }
-  if (!k_src || !v_src || !k_dst || !v_dst || !src.indptr || !src.indices || !d_fresh ||
-      !d_dst_indptr || !d_dst_indices)
+  // the source slots are read only for surviving pages, the free list and the
+  // destination slots only for destination pages
+  if (!k_src || !v_src || !k_dst || !v_dst || !src.indptr || !d_dst_indptr ||
+      (units > 0 && !src.indices) || (n_dst > 0 && (!d_fresh || !d_dst_indices)))
     return fail(SA_ERR_NULL, "a device pointer is NULL");
   if (!aligned16(k_src) || !aligned16(v_src) || !aligned16(k_dst) || !aligned16(v_dst))
     return fail(SA_ERR_ALIGN, "pool pointer not 16-byte aligned");
@@ -590,7 +592,8 @@ sa_status sa_kv_splice_alias(sa_ctx* ctx, const sa_layout* layout, int32_t batch
   sa_status s = plan_splice(layout, batch, h_src_len, h_keep_indptr, h_keep_spans, h_reserve, true,
                             num_fresh, dst_capacity, h_dst_len, sp);
   if (s != SA_OK) return s;
-  if (!src.indptr || !src.indices || !d_dst_indptr || !d_dst_indices || (sp.fresh_used > 0 && !d_fresh))
+  if (!src.indptr || !d_dst_indptr || (!sp.units.empty() && !src.indices) || (sp.n_dst > 0 && !d_dst_indices) ||
+      (sp.fresh_used > 0 && !d_fresh))
     return fail(SA_ERR_NULL, "a device pointer is NULL");
   s = check_ctx(ctx);
   if (s != SA_OK) return s;

@@ -159,14 +159,14 @@ def test_splice_alias_validation(lib):
     assert splice_alias(lib, L, [100], [1, 1], [[0, 7]], [10])[0] == 2           # indptr[0] != 0
 
 
-def assemble_append(lib, L, src_len, keep_indptr, spans, reserve, new_len, layer=0, k_new=FAKE):
+def assemble_append(lib, L, src_len, keep_indptr, spans, reserve, new_len, layer=0, k_new=FAKE, src_indices=FAKE):
     a = [np.asarray(x, dtype=np.int32) for x in (src_len, keep_indptr, np.asarray(spans).reshape(-1),
                                                   reserve, new_len)]
     out = np.zeros(len(a[0]), dtype=np.int32)
     return lib.sa_kv_assemble_append(None, ctypes.byref(L), FAKE, FAKE, FAKE, FAKE, len(a[0]),
                                      a[0].ctypes.data, a[1].ctypes.data,
                                      a[2].ctypes.data if a[2].size else None, a[3].ctypes.data,
-                                     sa._Pages(FAKE, FAKE), FAKE, 100, FAKE, FAKE, 100, out.ctypes.data,
+                                     sa._Pages(FAKE, src_indices), FAKE, 100, FAKE, FAKE, 100, out.ctypes.data,
                                      layer, k_new, FAKE, a[4].ctypes.data, None)
 
 
@@ -180,6 +180,11 @@ def test_assemble_append_validation(lib):
     assert assemble_append(lib, L, [100], [0, 1], [[0, 7]], [12], [4], k_new=None) == 1
     assert assemble_append(lib, L, [100], [0, 1], [[0, 7]], [12], [4], k_new=FAKE + 2) == 4
     assert assemble_append(lib, L, [100], [0, 2], [[0, 2], [1, 7]], [12], [4]) == 5   # overlap
+    # nothing cached: no source page is read, so the source slot list may be absent
+    assert assemble_append(lib, L, [0, 0], [0, 0, 0], [], [40, 3], [40, 3], src_indices=None) == 1
+    assert b"context" in lib.sa_last_error()
+    assert assemble_append(lib, L, [100], [0, 1], [[0, 7]], [12], [4], src_indices=None) == 1
+    assert b"NULL" in lib.sa_last_error()
 
 
 def test_context_creation_without_gpu(lib):

@@ -471,6 +471,52 @@ def test_splice_and_append_in_one_launch(ctx, name):
     check_lse(w, lse.cpu().numpy(), ref_lse)
 
 
+def random_case(k):
+    """Seeded small workload k: 1-5 sequences, prefixes 0..700 (partial pages included),
+    segments 1..300, 1-4 KV heads with G in {1, 2, 4, 8}, page 16 or 32; case 12 has no
+    prefixes, case 13 only whole-page ones."""
+    r = np.random.default_rng(7000 + k)
+    B = int(r.integers(1, 6))
+    Hkv = int(r.choice([1, 2, 4]))
+    G = int(r.choice([1, 2, 4, 8]))
+    P = int(r.choice([16, 32]))
+    pre = [int(x) for x in r.integers(0, 701, B)]
+    ql = [int(x) for x in r.integers(1, 301, B)]
+    if k == 12:
+        pre = [0] * B                                   # nothing cached: plain causal prefill
+    if k == 13:
+        pre = [P * int(x) for x in r.integers(1, 20, B)]  # prefixes that end on a page boundary
+    return build(f"rand{k}", 7000 + k, Hkv * G, Hkv, 128, P, pre, ql, assemble=True)
+
+
+@pytest.mark.parametrize("k", range(14))
+def test_random_small_steps(ctx, k):
+    """The benchmark step's launches (splice with the append in one launch, then the
+    attention) on seeded random shapes: destination table and kept lengths exact, every
+    output row and LSE against the oracle."""
+    w = random_case(k)
+    print(f"random step {k}: B {w.batch} Hq {w.num_q_heads} Hkv {w.num_kv_heads} P {w.page_size} "
+          f"pre {list(w.pre)} q {list(w.qlen)}", flush=True)
+    a = w.asm
+    L = layout_of(w)
+    kp, vp, sip, sid, fresh = build_source_cache(w)
+    dip = torch.zeros(w.batch + 1, dtype=torch.int32, device="cuda")
+    did = torch.full((len(a.fresh),), -1, dtype=torch.int32, device="cuda")
+    kept = sa.sa_kv_assemble_append(ctx, L, kp, vp, kp, vp, a.src_len, a.keep_indptr, a.keep_spans,
+                                    a.reserve, sip, sid, fresh, dip, did, 0, dev_u16(w.k_seg()),
+                                    dev_u16(w.v_seg()), w.qlen)
+    o, lse = attention(ctx, w, L, dev_u16(w.q), kp, vp, dip, did)
+    sa.sa_sync_check(ctx)
+    r = opages.assemble(a.src_len, a.src_indptr, a.src_indices, a.keep_indptr, a.keep_spans,
+                        a.reserve, a.fresh, w.page_size)
+    assert np.array_equal(kept, w.pre) and np.array_equal(kept, r["dst_len"])
+    assert np.array_equal(dip.cpu().numpy(), r["dst_indptr"])
+    assert np.array_equal(did.cpu().numpy()[: r["dst_indptr"][-1]], r["dst_indices"])
+    ref, ref_lse, _ = oracle_all(w)
+    compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
+    check_lse(w, lse.cpu().numpy(), ref_lse)
+
+
 @pytest.mark.timeout(600)
 def test_step_c2_full(ctx):
     print("c2 full step", flush=True)
