@@ -517,6 +517,29 @@ def test_random_small_steps(ctx, k):
     check_lse(w, lse.cpu().numpy(), ref_lse)
 
 
+@pytest.mark.parametrize("k", range(8))
+def test_random_mixed_attention(ctx, k):
+    """Seeded batches mixing decode rows (q = 1) and prefill segments over prefixes up to 6000
+    tokens; with few work items the planner splits long ones by key range and merges the
+    parts, so both paths meet shapes no fixed case has.  Every row and LSE vs the oracle."""
+    r = np.random.default_rng(9000 + k)
+    B = int(r.integers(1, 7))
+    Hkv = int(r.choice([1, 2, 4]))
+    G = int(r.choice([1, 2, 4, 8]))
+    P = int(r.choice([16, 32]))
+    pre = [int(x) for x in r.integers(0, 6001, B)]
+    ql = [1 if r.random() < 0.5 else int(r.integers(2, 201)) for _ in range(B)]
+    w = build(f"mixed{k}", 9000 + k, Hkv * G, Hkv, 128, P, pre, ql)
+    print(f"random mixed {k}: Hq {w.num_q_heads} Hkv {Hkv} P {P} pre {pre} q {ql}", flush=True)
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    o, lse = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    sa.sa_sync_check(ctx)
+    ref, ref_lse, _ = oracle_all(w)
+    compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
+    check_lse(w, lse.cpu().numpy(), ref_lse)
+
+
 @pytest.mark.timeout(600)
 def test_step_c2_full(ctx):
     print("c2 full step", flush=True)
