@@ -82,6 +82,18 @@ print("append in attention, split", flush=True)
 check_attention_append(ctx, build("split", 21, 8, 1, 128, 16, [5000, 3000, 70, 0], [1, 1, 3, 1]))
 print("append in attention, missing page", flush=True)
 test_append_inside_attention_missing_page_is_reported(ctx)
+from test_gpu_parity import random_case
+import numpy as np
+for k in range(6):
+    print("append in attention, random shape", k, flush=True)
+    check_attention_append(ctx, random_case(k), launches=1)
+for k in range(4):
+    r = np.random.default_rng(9100 + k)
+    B = int(r.integers(2, 7))
+    pre = [int(x) for x in r.integers(0, 4001, B)]
+    ql = [1 if r.random() < 0.5 else int(r.integers(2, 201)) for _ in range(B)]
+    print("append in attention, mixed decode/prefill", k, pre, ql, flush=True)
+    check_attention_append(ctx, build("amix%d" % k, 9100 + k, 16, 4, 128, 16, pre, ql), launches=1)
 print("append in attention, c2 step", flush=True)
 check_step(ctx, workloads.make("c2"), per_seq_rows=128, mode="attn_append")
 print("append in attention, c5", flush=True)
