@@ -10,6 +10,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <string>
+#include <map>
 #include <vector>
 
 #include "sa.h"
@@ -693,6 +694,7 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
     int64_t tiles;
     bool decode;
     int xcd;
+    int64_t group_tiles = 0;   // longest item of its (sequence, KV head)
   };
   std::vector<Work> work;
   int64_t total_tiles = 0;
@@ -738,8 +740,23 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
     }
     work.swap(split);
   }
-  std::stable_sort(work.begin(), work.end(), [](const Work& x, const Work& y) {
+  // Order: decode work first; then the items of one (sequence, KV head) next to
+  // each other, so that they run together on their XCD and read that
+  // sequence's K/V tiles through its L2 once, groups by their longest item
+  // and items within a group longest first.
+  {
+    std::map<int64_t, int64_t> group_len;                       // (seq, kvh) -> longest item
+    for (const Work& w : work) {
+      int64_t& g = group_len[(int64_t)w.it.seq * Hkv + w.it.kvh];
+      g = std::max(g, w.tiles);
+    }
+    for (Work& w : work) w.group_tiles = group_len[(int64_t)w.it.seq * Hkv + w.it.kvh];
+  }
+  std::stable_sort(work.begin(), work.end(), [Hkv](const Work& x, const Work& y) {
     if (x.decode != y.decode) return x.decode;
+    if (x.group_tiles != y.group_tiles) return x.group_tiles > y.group_tiles;
+    const int64_t gx = (int64_t)x.it.seq * Hkv + x.it.kvh, gy = (int64_t)y.it.seq * Hkv + y.it.kvh;
+    if (gx != gy) return gx < gy;
     return x.tiles > y.tiles;
   });
   // XCD-aware placement: block i runs on XCD i % 8, so all items of one

@@ -159,6 +159,9 @@ def run(out_path=None):
              for _ in range(2)]
     rec = {"layout": "Hq 32 / Hkv 8 / d 128, page 16, bf16", "profile": [], "mixed": []}
     with sa.Context(0) as ctx:
+        # the shader clock takes tens of milliseconds of load to settle: warm up on the
+        # largest profiling batch (~50 ms) before any launch is timed
+        _time_launch(sa, ctx, L, pools, [256] * 4, [16384 + 256] * 4, reps=200, warmup=0)
         prof_w, prof_t = [], []
         for name, q, kv in profiling_batches():
             t = _time_launch(sa, ctx, L, pools, q, kv)
