@@ -694,7 +694,8 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
     int64_t tiles;
     bool decode;
     int xcd;
-    int64_t group_tiles = 0;   // longest item of its (sequence, KV head)
+    int64_t group = 0;         // items that stay together in the launch order
+    int64_t group_tiles = 0;   // the longest item of that group
   };
   std::vector<Work> work;
   int64_t total_tiles = 0;
@@ -740,23 +741,35 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
     }
     work.swap(split);
   }
-  // Order: decode work first; then the items of one (sequence, KV head) next to
-  // each other, so that they run together on their XCD and read that
-  // sequence's K/V tiles through its L2 once, groups by their longest item
-  // and items within a group longest first.
+  // Order: decode work first, then longest first, except that the row tiles of
+  // one (sequence, KV head) prefill stay next to each other (ranked by the
+  // group's longest tile): they read the same K/V range, so run together on
+  // their XCD they stream it through its L2 once.  Decode items and the
+  // key-range parts of split items share no K/V with their neighbours and
+  // keep the plain longest-first order.
   {
-    std::map<int64_t, int64_t> group_len;                       // (seq, kvh) -> longest item
-    for (const Work& w : work) {
-      int64_t& g = group_len[(int64_t)w.it.seq * Hkv + w.it.kvh];
-      g = std::max(g, w.tiles);
+    std::map<int64_t, int64_t> group_len;                       // (seq, kvh) -> longest row tile
+    auto grouped = [](const Work& w) { return !w.decode && w.it.part < 0; };
+    for (const Work& w : work)
+      if (grouped(w)) {
+        int64_t& g = group_len[(int64_t)w.it.seq * Hkv + w.it.kvh];
+        g = std::max(g, w.tiles);
+      }
+    for (size_t i = 0; i < work.size(); ++i) {
+      Work& w = work[i];
+      if (grouped(w)) {
+        w.group = (int64_t)w.it.seq * Hkv + w.it.kvh;
+        w.group_tiles = group_len[w.group];
+      } else {
+        w.group = (int64_t)i - (int64_t)work.size();              // a group of its own, in list order
+        w.group_tiles = w.tiles;
+      }
     }
-    for (Work& w : work) w.group_tiles = group_len[(int64_t)w.it.seq * Hkv + w.it.kvh];
   }
-  std::stable_sort(work.begin(), work.end(), [Hkv](const Work& x, const Work& y) {
+  std::stable_sort(work.begin(), work.end(), [](const Work& x, const Work& y) {
     if (x.decode != y.decode) return x.decode;
     if (x.group_tiles != y.group_tiles) return x.group_tiles > y.group_tiles;
-    const int64_t gx = (int64_t)x.it.seq * Hkv + x.it.kvh, gy = (int64_t)y.it.seq * Hkv + y.it.kvh;
-    if (gx != gy) return gx < gy;
+    if (x.group != y.group) return x.group < y.group;
     return x.tiles > y.tiles;
   });
   // XCD-aware placement: block i runs on XCD i % 8, so all items of one
