@@ -433,21 +433,24 @@ def test_step_small_fused(ctx, name, mode):
     check_step(ctx, small(name), per_seq_rows=64, mode=mode)
 
 
+@pytest.mark.parametrize("layers,layer", [(1, 0), (2, 1)])
 @pytest.mark.parametrize("name", WITH_ASM)
-def test_splice_and_append_in_one_launch(ctx, name):
-    """sa_kv_assemble_append leaves both pools exactly as the oracle's splice
-    (whole pages copied) followed by its append -- including the rows of a
-    partial last surviving page that the segment fills and those it does not."""
-    print(f"splice+append {name}", flush=True)
+def test_splice_and_append_in_one_launch(ctx, name, layers, layer):
+    """sa_kv_assemble_append leaves both pools exactly as the oracle's splice (whole
+    pages copied, in every layer) followed by its append (in the given layer only) --
+    including the rows of a partial last surviving page that the segment fills and
+    those it does not.  With the append in layer 0 the attention over the result is
+    checked too (the other layers hold bit-flipped copies of the rows)."""
+    print(f"splice+append {name}, {layers} layers, append in layer {layer}", flush=True)
     w = small(name)
     a = w.asm
-    L = layout_of(w)
-    kp, vp, sip, sid, fresh = build_source_cache(w)
-    want_k, want_v = host_u16(kp[0]).copy(), host_u16(vp[0]).copy()
+    L = layout_of(w, num_layers=layers)
+    kp, vp, sip, sid, fresh = build_source_cache(w, num_layers=layers)
+    want_k, want_v = host_u16(kp).copy(), host_u16(vp).copy()
     dip = torch.zeros(w.batch + 1, dtype=torch.int32, device="cuda")
     did = torch.full((len(a.fresh),), -1, dtype=torch.int32, device="cuda")
     kept = sa.sa_kv_assemble_append(ctx, L, kp, vp, kp, vp, a.src_len, a.keep_indptr, a.keep_spans,
-                                    a.reserve, sip, sid, fresh, dip, did, 0, dev_u16(w.k_seg()),
+                                    a.reserve, sip, sid, fresh, dip, did, layer, dev_u16(w.k_seg()),
                                     dev_u16(w.v_seg()), w.qlen)
     sa.sa_sync_check(ctx)
     r = opages.assemble(a.src_len, a.src_indptr, a.src_indices, a.keep_indptr, a.keep_spans,
@@ -458,18 +461,20 @@ def test_splice_and_append_in_one_launch(ctx, name):
     sl, ro = opages.append_destinations(r["dst_len"], w.qlen, r["dst_indptr"], r["dst_indices"],
                                         w.page_size)
     for want, seg in ((want_k, w.k_seg()), (want_v, w.v_seg())):
-        for s_, d_ in zip(r["copy_src"], r["copy_dst"]):
-            want[d_] = want[s_]
-        opages.apply_append(want, seg, sl, ro)
-    assert np.array_equal(host_u16(kp[0]), want_k)
-    assert np.array_equal(host_u16(vp[0]), want_v)
+        for lay in range(layers):
+            for s_, d_ in zip(r["copy_src"], r["copy_dst"]):
+                want[lay, d_] = want[lay, s_]
+        opages.apply_append(want[layer], seg, sl, ro)
+    assert np.array_equal(host_u16(kp), want_k)
+    assert np.array_equal(host_u16(vp), want_v)
     assert any(int(x) % w.page_size for x in r["dst_len"])    # a partial last page was exercised
+    if layer != 0:
+        return
     o, lse = attention(ctx, w, L, dev_u16(w.q), kp, vp, dip, did)
     sa.sa_sync_check(ctx)
     ref, ref_lse, _ = oracle_all(w)
     compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
     check_lse(w, lse.cpu().numpy(), ref_lse)
-
 
 def random_case(k):
     """Seeded small workload k: 1-5 sequences, prefixes 0..700 (partial pages included),
