@@ -20,7 +20,7 @@
 // use) comes out of the MFMA itself: the query rows are scaled by c once, when
 // they are loaded, and every S accumulation starts from -m instead of zero.
 // That takes the 32 fma per lane and tile off the VALU.  The price is one
-// more bf16 rounding, of c q: each x moves by at most 2^-9 sum_d |c q_d k_d|,
+// more bf16 rounding, of c q: each x moves by at most 2^-8 sum_d |c q_d k_d|,
 // so the log-sum-exp moves by at most ln 2 times that, over the row's keys;
 // the output's own error stays far inside its tolerance.
 #pragma once

@@ -17,7 +17,7 @@ from workloads.configs import build, source_rows
 
 from harness import (attention, build_cache, build_source_cache, compare, dev_i32, dev_u16,
                      host_u16, layout_of, lse_tolerance, new_pool, place_range, run_assemble,
-                     sample_rows)
+                     sample_rows, score_shift_bound)
 
 
 def check_lse(w, got, ref, toks=None, heads=None):
@@ -260,6 +260,36 @@ def test_constant_values_and_zero_keys_closed_forms(ctx):
         for i in range(int(w.qlen[b])):
             want = np.repeat(run[pre + i], G, axis=0)            # [Hq][D]
             compare(bits[int(w.q_indptr[b]) + i], want, MAX_TOL, MEAN_TOL)
+
+
+@pytest.mark.parametrize("scale,std", [(1.0, 1.0), (2.0, 1.0), (1e-4, 1.0)])
+def test_large_and_tiny_softmax_scales(ctx, scale, std):
+    """Scores spread over tens of powers of two (the running max keeps moving past the
+    lazy-rescale threshold) and nearly uniform weights.  The kernel rounds c q to bf16,
+    so each row's exponents may move by eps = 2^-8 max_j sum_d |c q_d k_jd|: its LSE must
+    stay within ln 2 eps of the oracle's and each output within (2^(2 eps) - 1) max|v| plus
+    the bf16 roundings of P and O (2^-7 max|v|) -- a missed rescale or an overflow would
+    be off by factors of 2^8 or not finite."""
+    w = build(f"scale{scale}", 64, 8, 2, 128, 16, [700, 0, 33], [150, 90, 1], std=std)
+    w.scale = scale
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    o, lse = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    sa.sa_sync_check(ctx)
+    ref, ref_lse, _ = oracle_all(w)
+    got = (host_u16(o).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    assert np.isfinite(got).all() and np.isfinite(lse.cpu().numpy()).all()
+    check_lse(w, lse.cpu().numpy(), ref_lse)
+    T = int(w.q_indptr[-1])
+    toks = np.repeat(np.arange(T, dtype=np.int64), w.num_q_heads)
+    heads = np.tile(np.arange(w.num_q_heads, dtype=np.int32), T)
+    eps = 2.0 ** -8 * score_shift_bound(w, toks, heads)
+    vmax = np.abs((w.v.astype(np.uint32) << 16).view(np.float32)).max()
+    tol = (2.0 ** (2 * eps) - 1.0) * vmax + 2.0 ** -7 * vmax + 1e-3
+    err = np.abs(got - ref).reshape(T * w.num_q_heads, -1).max(axis=1)
+    assert (err <= tol).all(), float((err - tol).max())
+    if scale < 1e-3:
+        compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
 
 
 def test_page_permutation_invariance(ctx):
