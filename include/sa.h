@@ -235,7 +235,10 @@ sa_status sa_kv_splice_alias(sa_ctx *ctx, const sa_layout *layout, int32_t batch
  * rows are bf16 (round to nearest even); `lse` may be NULL.  Sequences with
  * h_q_len[b] == 0 are skipped.  Arithmetic: bf16 MFMA products with fp32
  * accumulation, fp32 online softmax, probabilities rounded to bf16 before the
- * PV product.
+ * PV product.  The default kernel multiplies each query row by
+ * softmax_scale * log2(e) once and rounds it to bf16, which moves a row's
+ * scaled scores by at most 2^-8 * sum_d |scale log2(e) q_d k_d| (log2 units);
+ * with SA_ATTN_VARIANT=1 the scale is applied in fp32 instead (slower).
  *
  * Errors: SA_ERR_SHAPE (0 <= q_len <= kv_len violated, bad batch or layer,
  * softmax_scale not finite and positive),
