@@ -48,6 +48,8 @@ def parse():
     p.add_argument("--rotate", type=int, default=8, help="disjoint cache copies cycled per step")
     p.add_argument("--fuse", choices=("attn", "splice", "none"), default="splice",
                    help="which launch carries the append (see the module docstring)")
+    p.add_argument("--exact-scale", action="store_true",
+                   help="apply the softmax scale to each score in fp32 (sa_set_exact_scale)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-stride", type=int, default=1, help="oracle sample: every n-th token")
     p.add_argument("--assemble-layers", type=int, default=32,
@@ -129,6 +131,8 @@ def config_mode(args):
     o = torch.empty((T, Hq, 128), dtype=torch.int16, device="cuda")
     lse = torch.empty((T, Hq), dtype=torch.float32, device="cuda")
     ctx = sa.Context(0)
+    if args.exact_scale:
+        sa.sa_set_exact_scale(ctx, True)
     stream = torch.cuda.current_stream()
     app_bytes = 2 * T * Hkv * 128 * 2 * 2
     a = w.asm
@@ -286,6 +290,8 @@ def main():
     o = torch.empty((T, w.num_q_heads, 128), dtype=torch.int16, device="cuda")
     lse = torch.empty((T, w.num_q_heads), dtype=torch.float32, device="cuda")
     ctx = sa.Context(0)
+    if args.exact_scale:
+        sa.sa_set_exact_scale(ctx, True)
     stream = torch.cuda.current_stream()
     fuse = args.fuse
 
@@ -385,6 +391,7 @@ def main():
                         "causal GQA over 8192 + 2048",
             "batch": 1, "prefix": int(w.pre[0]), "segment": T, "page_size": P,
             "cache_copies_rotated": R,
+            "softmax_scale": "per score, fp32" if args.exact_scale else "folded into q (bf16)",
         },
         "attn": {"ms": attn_ms, "gflop": flops / 1e9, "tflops": attn_tflops,
                  "frac_of_bf16_peak": attn_tflops / PEAK_BF16_TFLOPS,

@@ -15,7 +15,7 @@ import numpy as np
 __all__ = [
     "Layout", "Context", "SaError", "library_path", "load_library",
     "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append", "sa_kv_splice_alias",
-    "sa_segment_prefill_attn", "sa_segment_prefill_attn_append", "sa_sync_check",
+    "sa_segment_prefill_attn", "sa_segment_prefill_attn_append", "sa_set_exact_scale", "sa_sync_check",
     "EXPORTED_SYMBOLS",
 ]
 
@@ -25,7 +25,8 @@ _lib = None
 
 EXPORTED_SYMBOLS = ("sa_create", "sa_destroy", "sa_status_string", "sa_last_error",
                     "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
-                    "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append")
+                    "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append",
+                    "sa_set_exact_scale")
 
 STATUS = {0: "SA_OK", 1: "SA_ERR_NULL", 2: "SA_ERR_SHAPE", 3: "SA_ERR_UNSUPPORTED",
           4: "SA_ERR_ALIGN", 5: "SA_ERR_RANGE", 6: "SA_ERR_NO_PAGES", 7: "SA_ERR_HIP",
@@ -81,8 +82,10 @@ def load_library():
                                             P, P, P]
     lib.sa_segment_prefill_attn_append.argtypes = [P, LP, I32, P, P, P, P, P, I32, P, P, _Pages,
                                                    ctypes.c_float, P, P, P]
+    lib.sa_set_exact_scale.argtypes = [P, I32]
     for name in ("sa_create", "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
-                 "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append"):
+                 "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append",
+                 "sa_set_exact_scale"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -248,6 +251,12 @@ def sa_segment_prefill_attn(ctx, layout: Layout, layer: int, q, k_pool, v_pool, 
         _ctx_handle(ctx), ctypes.byref(layout), int(layer), _ptr(q), _ptr(k_pool), _ptr(v_pool),
         int(len(q_len)), _ptr(q_len), _ptr(kv_len), _pages(pages_indptr, pages_indices),
         float(softmax_scale), _ptr(o), _ptr(lse), _stream(stream)))
+
+
+def sa_set_exact_scale(ctx, enable: bool = True):
+    """Later attention calls on ctx apply the softmax scale to each score in fp32
+    (enable) or fold it into the bf16 query rows (the default)."""
+    _check(load_library().sa_set_exact_scale(_ctx_handle(ctx), int(bool(enable))))
 
 
 def sa_segment_prefill_attn_append(ctx, layout: Layout, layer: int, q, k_pool, v_pool, k_new, v_new, q_len,

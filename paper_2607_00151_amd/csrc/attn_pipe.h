@@ -22,7 +22,9 @@
 // That takes the 32 fma per lane and tile off the VALU.  The price is one
 // more bf16 rounding, of c q: each x moves by at most 2^-8 sum_d |c q_d k_d|,
 // so the log-sum-exp moves by at most ln 2 times that, over the row's keys;
-// the output's own error stays far inside its tolerance.
+// at moderate logits the output's own error stays far inside its tolerance.
+// The exact-scale form (kExact) keeps q as given, starts the accumulations
+// from zero and computes each exponent as fma(s, c, -m) in fp32.
 #pragma once
 
 #include "attn_kernel.h"
@@ -205,7 +207,7 @@ __device__ __forceinline__ void app_finish(const AttnArgs& a) {
 // kPoolRsrc: a layer's K (and V) pool spans < 2^31 bytes, so one buffer
 // resource per pool reaches every page through the 32-bit scalar offset;
 // otherwise each page load builds a resource for its page.
-template <int P, bool kPoolRsrc, int kGroups, int GRP, bool kApp = false>
+template <int P, bool kPoolRsrc, int kGroups, int GRP, bool kApp = false, bool kExact = false>
 __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs& a, const AttnItem& it,
                                                                  const SeqDesc& sd, const PipeLds& L) {
   static_assert(P == 16 || P == 32, "page size");
@@ -376,10 +378,16 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
     const int g = j >> 2;
     return X[g >> 1][8 * (g & 1) + 2 * (j & 3) + h];
   };
+  // probability of one score: the accumulator holds x - m already, or (exact
+  // scale) the raw q.k, which is scaled and offset here in fp32
+  auto xexp = [&](float v) __attribute__((always_inline)) {
+    if constexpr (kExact) return exp2f_fast(__builtin_fmaf(v, a.c, -msub));
+    else return exp2f_fast(v);
+  };
   auto exp_pair = [&](const f32x16* X, int j) __attribute__((always_inline)) {
     const int g = j >> 2, e = 2 * (j & 3);
-    const float p0 = exp2f_fast(xpair(X, j, 0));
-    const float p1 = exp2f_fast(xpair(X, j, 1));
+    const float p0 = xexp(xpair(X, j, 0));
+    const float p1 = xexp(xpair(X, j, 1));
     pop[g][e] = (__bf16)p0;
     pop[g][e + 1] = (__bf16)p1;
     return p0 + p1;
@@ -400,7 +408,7 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
   // shift the tile's x values to the new offset
   auto rescale_test = [&](float mx, f32x16* X) __attribute__((always_inline)) {
     mx = pair_max(mx);
-    const float cand = mx + msub;                           // c * row max
+    const float cand = kExact ? mx * a.c : mx + msub;       // c * row max
     if (__ballot(cand > m_used + kRescaleLog2)) {
       const float m_new = fmaxf(m_used, cand);
       const float alpha = (m_new == -INFINITY) ? 1.f : exp2f_fast(m_used - m_new);
@@ -408,17 +416,27 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
       const float msub_new = (m_used == -INFINITY) ? 0.f : m_used;
       const float shift = msub_new - msub;
       msub = msub_new;
+      // the accumulators start from the new offset (x values only; exact-scale
+      // scores carry no offset)
+      if constexpr (!kExact) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) negm[e] = -msub;
+        for (int e = 0; e < 16; ++e) negm[e] = -msub;
+      }
       l *= alpha;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
         for (int e = 0; e < 16; ++e) oacc[dt][e] *= alpha;
+      if constexpr (!kExact) {
+        // and the tile's x values move to it
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+        for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) X[kt][e] -= shift;
+          for (int e = 0; e < 16; ++e) X[kt][e] -= shift;
+      } else {
+        (void)shift;
+        (void)X;
+      }
     }
   };
   auto row_max = [&](const f32x16* S) __attribute__((always_inline)) {
@@ -500,8 +518,8 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
     float ls[2] = {0.f, 0.f};   // two accumulation chains for the denominator
 #pragma unroll
     for (int i = 0; i < kAhead; ++i) kop[i] = read_k(kb, i);
-    ex[0][0] = exp2f_fast(xpair(sc[B], 0, 0));
-    ex[0][1] = exp2f_fast(xpair(sc[B], 0, 1));
+    ex[0][0] = xexp(xpair(sc[B], 0, 0));
+    ex[0][1] = xexp(xpair(sc[B], 0, 1));
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       if (i + kAhead < 16) kop[i + kAhead] = read_k(kb, i + kAhead);
@@ -509,8 +527,8 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
       else if (i < 2 * kNJ) tile_load(s_a, vbase, rsrc_v, voff, vn, i - kNJ);
       s_step(sc[N], kop[i], i);
       if (i + 1 < 16) {
-        ex[i + 1][0] = exp2f_fast(xpair(sc[B], i + 1, 0));
-        ex[i + 1][1] = exp2f_fast(xpair(sc[B], i + 1, 1));
+        ex[i + 1][0] = xexp(xpair(sc[B], i + 1, 0));
+        ex[i + 1][1] = xexp(xpair(sc[B], i + 1, 1));
       }
       ls[i & 1] += ex[i][0] + ex[i][1];
       pop[i >> 2][2 * (i & 3)] = (__bf16)ex[i][0];
@@ -586,7 +604,8 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
 #pragma unroll
   for (int ks = 0; ks < 8; ++ks)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) qop[ks][e] = (__bf16)((float)qop[ks][e] * a.c);
+    for (int e = 0; e < 8; ++e)
+      if constexpr (!kExact) qop[ks][e] = (__bf16)((float)qop[ks][e] * a.c);
   __builtin_amdgcn_s_waitcnt(0x0070);
   lds_barrier();
   if (kGroups == 2 && GRP == 1) lds_barrier();             // group 1 runs a barrier behind
@@ -761,7 +780,9 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
 
 // One group of four waves per block, two blocks per CU.
 // kApp: the launch also writes the segment's new K/V rows (app_produce).
-template <int P, bool kPoolRsrc, bool kApp>
+// kExact: the softmax scale is applied in fp32 to each score instead of to
+// the query rows in bf16 (one fma per score; no rounding of c q).
+template <int P, bool kPoolRsrc, bool kApp, bool kExact = false>
 __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t k_lds0[kTileBytes], k_lds1[kTileBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t v_lds0[kTileBytes], v_lds1[kTileBytes];
@@ -771,7 +792,7 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
     const SeqDesc sd{it.q_start, it.q_len, it.kv_len, 0};
     const PipeLds L{(lds_u8*)k_lds0, (lds_u8*)k_lds1, (lds_u8*)v_lds0, (lds_u8*)v_lds1,
                     nullptr, nullptr, nullptr, nullptr, nullptr};
-    pipe_group<P, kPoolRsrc, 1, 0, kApp>(a, it, sd, L);
+    pipe_group<P, kPoolRsrc, 1, 0, kApp, kExact>(a, it, sd, L);
   }
   if constexpr (kApp) app_finish(a);
 }

@@ -83,6 +83,7 @@ struct sa_ctx {
   float* part = nullptr;           // split-KV partials
   size_t part_cap = 0;             // bytes
   uint32_t* d_sync = nullptr;      // counters of an attention launch that appends (zero between launches)
+  bool exact_scale = false;        // sa_set_exact_scale
 };
 
 namespace {
@@ -192,8 +193,12 @@ bool append_in_attention() {
 }
 
 template <int P>
-void launch_attn_p(AttnVariant v, bool pool_rsrc, dim3 grid, hipStream_t st, const sa::AttnArgs& a) {
-  if (v.pipe == 2 && pool_rsrc)
+void launch_attn_p(AttnVariant v, bool pool_rsrc, bool exact, dim3 grid, hipStream_t st, const sa::AttnArgs& a) {
+  if (v.pipe == 1 && exact && pool_rsrc)
+    hipLaunchKernelGGL((sa::attn_pipe_kernel<P, true, false, true>), grid, dim3(256), 0, st, a);
+  else if (v.pipe == 1 && exact)
+    hipLaunchKernelGGL((sa::attn_pipe_kernel<P, false, false, true>), grid, dim3(256), 0, st, a);
+  else if (v.pipe == 2 && pool_rsrc)
     hipLaunchKernelGGL((sa::attn_pp_kernel<P, true>), grid, dim3(512), 0, st, a);
   else if (v.pipe == 2)
     hipLaunchKernelGGL((sa::attn_pp_kernel<P, false>), grid, dim3(512), 0, st, a);
@@ -211,9 +216,10 @@ void launch_attn_p(AttnVariant v, bool pool_rsrc, dim3 grid, hipStream_t st, con
 
 // pool_rsrc: a layer's K (and V) pool spans < 2^31 bytes, so one buffer
 // resource per pool addresses every page with a 32-bit offset
-void launch_attn(int page_size, AttnVariant v, bool pool_rsrc, dim3 grid, hipStream_t st, const sa::AttnArgs& a) {
-  if (page_size == 16) launch_attn_p<16>(v, pool_rsrc, grid, st, a);
-  else launch_attn_p<32>(v, pool_rsrc, grid, st, a);
+void launch_attn(int page_size, AttnVariant v, bool pool_rsrc, bool exact, dim3 grid, hipStream_t st,
+                 const sa::AttnArgs& a) {
+  if (page_size == 16) launch_attn_p<16>(v, pool_rsrc, exact, grid, st, a);
+  else launch_attn_p<32>(v, pool_rsrc, exact, grid, st, a);
 }
 
 }  // namespace
@@ -677,7 +683,9 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
 
   // ---- kernel variant: query rows per wave (32 * qt) and waves per work item
   const AttnVariant var = attn_variant();
-  const bool fused = append && var.pipe == 1 && append_in_attention();
+  // the exact-scale form of the pipelined kernel has no in-launch append
+  const bool exact = ctx->exact_scale && var.pipe == 1;
+  const bool fused = append && var.pipe == 1 && !exact && append_in_attention();
   if (append && !fused) {
     // the new rows go in with an append launch of their own
     std::vector<int32_t> start(batch);
@@ -882,7 +890,7 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
     a.app_tickets = (int32_t)tickets;
   }
   const bool pool_rsrc = layer_elems(layout) * 2 < ((int64_t)1 << 31);
-  launch_attn(layout->page_size, var, pool_rsrc, dim3((unsigned)items.size()), (hipStream_t)stream, a);
+  launch_attn(layout->page_size, var, pool_rsrc, exact, dim3((unsigned)items.size()), (hipStream_t)stream, a);
   SA_HIP(hipGetLastError());
   if (!groups.empty()) {
     sa::MergeArgs m{};
@@ -913,6 +921,13 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
                                   void* stream) {
   return attn_launch(ctx, layout, layer, q, k_pool, v_pool, false, nullptr, nullptr, batch, h_q_len,
                      h_kv_len, pages, softmax_scale, o, lse, stream);
+}
+
+sa_status sa_set_exact_scale(sa_ctx* ctx, int32_t enable) {
+  sa_status s = check_ctx(ctx);
+  if (s != SA_OK) return s;
+  ctx->exact_scale = enable != 0;
+  return SA_OK;
 }
 
 sa_status sa_segment_prefill_attn_append(sa_ctx* ctx, const sa_layout* layout, int32_t layer,

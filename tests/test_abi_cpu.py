@@ -82,6 +82,11 @@ def attn_append(lib, L, q_len, kv_len, k_new=FAKE, v_new=FAKE, layer=0):
                                               sa._Pages(FAKE, FAKE), 0.1, FAKE, None, None)
 
 
+def test_exact_scale_needs_a_context(lib):
+    assert lib.sa_set_exact_scale(None, 1) == 1
+    assert b"context" in lib.sa_last_error()
+
+
 def test_attn_append_validation(lib):
     assert attn_append(lib, layout(), [4], [8]) == 1                # all valid -> NULL ctx
     assert b"context" in lib.sa_last_error()

@@ -292,6 +292,51 @@ def test_large_and_tiny_softmax_scales(ctx, scale, std):
         compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
 
 
+@pytest.fixture(scope="module")
+def ctx_exact():
+    c = sa.Context(0)
+    sa.sa_set_exact_scale(c, True)
+    yield c
+    c.close()
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_exact_scale_all_rows(ctx_exact, name):
+    """The pipelined kernel with the scale applied per score in fp32: same bars, and the
+    LSE within 1e-4 of the oracle (no rounding of the scaled query to allow for)."""
+    w = small(name)
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    o, lse = attention(ctx_exact, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    sa.sa_sync_check(ctx_exact)
+    ref, ref_lse, _ = oracle_all(w)
+    compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() <= 1e-4
+
+
+@pytest.mark.parametrize("scale", [1.0, 2.0, 1e-4])
+def test_exact_scale_at_large_and_tiny_scales(ctx_exact, scale):
+    """Exact scaling keeps the LSE within 1e-4 of the oracle where the folded scale moves
+    it by up to ~0.16; the outputs are then off by the bf16 roundings of P and O only."""
+    w = build(f"xscale{scale}", 64, 8, 2, 128, 16, [700, 0, 33], [150, 90, 1], std=1.0)
+    w.scale = scale
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    o, lse = attention(ctx_exact, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    sa.sa_sync_check(ctx_exact)
+    ref, ref_lse, _ = oracle_all(w)
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() <= 1e-4
+    got = (host_u16(o).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    vmax = np.abs((w.v.astype(np.uint32) << 16).view(np.float32)).max()
+    assert np.abs(got - ref).max() <= 2.0 ** -6 * vmax
+
+
+@pytest.mark.timeout(600)
+def test_exact_scale_step_c2_full(ctx_exact):
+    print("c2 full step, exact scale", flush=True)
+    check_step(ctx_exact, workloads.make("c2"), per_seq_rows=128)
+
+
 def test_page_permutation_invariance(ctx):
     """Where the pages sit in the pool does not change a single output bit."""
     w = workloads.make("c1")
