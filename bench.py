@@ -51,6 +51,8 @@ def parse():
     p.add_argument("--exact-scale", action="store_true",
                    help="apply the softmax scale to each score in fp32 (sa_set_exact_scale)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-gemm-reference", action="store_true",
+                   help="skip timing torch's bf16 GEMM (context for the MFMA roofline)")
     p.add_argument("--cpu-stride", type=int, default=1, help="oracle sample: every n-th token")
     p.add_argument("--assemble-layers", type=int, default=32,
                    help="layers of the separate all-layer assemble measurement (0: skip)")
@@ -89,6 +91,28 @@ def stored_traffic(kernel: str, algorithmic: float):
     write = k["write_kib_per_launch"] * 1024 * t["copy_calibration"]["write_factor"]
     return {"bytes": fetch + write, "fetch_bytes": fetch, "write_bytes": write,
             "algorithmic_bytes": algorithmic, "ratio_to_algorithmic": (fetch + write) / algorithmic}
+
+
+def gemm_reference(n: int = 8192, reps: int = 30):
+    """Context for the MFMA roofline: torch's own bf16 GEMM (hipBLASLt) of
+    n x n x n on the same GPU, in the same run."""
+    import torch
+    a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    for _ in range(10):
+        c = a @ b
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(reps):
+        c = a @ b
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / reps
+    tflops = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
+    del a, b, c
+    return {"kind": f"torch.matmul bf16 {n}x{n}x{n} (hipBLASLt)", "ms": ms, "tflops": tflops,
+            "frac_of_bf16_peak": tflops / PEAK_BF16_TFLOPS}
 
 
 def copy_mode(nbytes: int, steps: int, warmup: int):
@@ -398,10 +422,17 @@ def main():
                  "tokens_per_s": T / (attn_ms * 1e-3)},
         "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": attn_tflops / PEAK_BF16_TFLOPS,
-                     "traffic": stored_traffic("attn_pipe_kernel", attn_bytes)},
+                     "traffic": None},
         "paper_context": "paper reports up to 11.9x transform-point TTFT reduction end to end on "
                          "H100 80GB (SGLang, Qwen3-8B); no kernel-level numbers",
     }
+
+    traffic = stored_traffic("attn_pipe_kernel", attn_bytes)
+    if traffic is not None:
+        rec["roofline"]["traffic"] = traffic["bytes"]
+        rec["roofline"]["traffic_detail"] = traffic
+    if not args.no_gemm_reference:
+        rec["gemm_reference"] = gemm_reference()
 
     in_attn = fuse == "attn" and os.environ.get("SA_APPEND_IN_ATTN") == "1"
     rec["config"]["launches"] = {"attn": "splice | append + attention" if in_attn else
