@@ -265,6 +265,29 @@ sa_status sa_segment_prefill_attn(sa_ctx *ctx, const sa_layout *layout, int32_t 
 sa_status sa_set_exact_scale(sa_ctx *ctx, int32_t enable);
 
 /*
+ * sa_set_kernel_events — timing hook for measurement.  While set for `which`,
+ * every kernel of that kind this context launches is launched by
+ * hipExtLaunchKernelGGL with start_event and stop_event (hipEvent_t handles
+ * the caller created with timing enabled), which binds both events to that
+ * kernel, so their elapsed time is the kernel's execution on the device
+ * rather than that of the call (events recorded around a call also span the
+ * dispatch gap, several microseconds).  Kinds:
+ *   SA_TIMED_ATTN   the attention kernel of sa_segment_prefill_attn and
+ *                   sa_segment_prefill_attn_append (not the partial merge
+ *                   that follows a launch split by key range)
+ *   SA_TIMED_PAGES  the page kernel of sa_kv_append, sa_kv_assemble,
+ *                   sa_kv_assemble_append, sa_kv_splice_alias and the append
+ *                   launch of sa_segment_prefill_attn_append
+ * A later launch of the same kind re-binds the same events.  Both NULL clears
+ * the hook; the events stay owned by the caller and must outlive the launches.
+ * Errors: SA_ERR_NULL for a NULL context or one event without the other,
+ * SA_ERR_SHAPE for an unknown kind.
+ */
+#define SA_TIMED_ATTN 0
+#define SA_TIMED_PAGES 1
+sa_status sa_set_kernel_events(sa_ctx *ctx, int32_t which, void *start_event, void *stop_event);
+
+/*
  * sa_segment_prefill_attn_append — the segment's append and its attention in
  * one call: each sequence's h_q_len[b] new K/V rows are written to its
  * logical positions h_kv_len[b] - h_q_len[b] .. h_kv_len[b] - 1 (as

@@ -15,8 +15,8 @@ import numpy as np
 __all__ = [
     "Layout", "Context", "SaError", "library_path", "load_library",
     "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append", "sa_kv_splice_alias",
-    "sa_segment_prefill_attn", "sa_segment_prefill_attn_append", "sa_set_exact_scale", "sa_sync_check",
-    "EXPORTED_SYMBOLS",
+    "sa_segment_prefill_attn", "sa_segment_prefill_attn_append", "sa_set_exact_scale", "sa_set_kernel_events",
+    "sa_sync_check", "EXPORTED_SYMBOLS",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -26,7 +26,7 @@ _lib = None
 EXPORTED_SYMBOLS = ("sa_create", "sa_destroy", "sa_status_string", "sa_last_error",
                     "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
                     "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append",
-                    "sa_set_exact_scale")
+                    "sa_set_exact_scale", "sa_set_kernel_events")
 
 STATUS = {0: "SA_OK", 1: "SA_ERR_NULL", 2: "SA_ERR_SHAPE", 3: "SA_ERR_UNSUPPORTED",
           4: "SA_ERR_ALIGN", 5: "SA_ERR_RANGE", 6: "SA_ERR_NO_PAGES", 7: "SA_ERR_HIP",
@@ -83,9 +83,10 @@ def load_library():
     lib.sa_segment_prefill_attn_append.argtypes = [P, LP, I32, P, P, P, P, P, I32, P, P, _Pages,
                                                    ctypes.c_float, P, P, P]
     lib.sa_set_exact_scale.argtypes = [P, I32]
+    lib.sa_set_kernel_events.argtypes = [P, I32, P, P]
     for name in ("sa_create", "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
                  "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append",
-                 "sa_set_exact_scale"):
+                 "sa_set_exact_scale", "sa_set_kernel_events"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -257,6 +258,17 @@ def sa_set_exact_scale(ctx, enable: bool = True):
     """Later attention calls on ctx apply the softmax scale to each score in fp32
     (enable) or fold it into the bf16 query rows (the default)."""
     _check(load_library().sa_set_exact_scale(_ctx_handle(ctx), int(bool(enable))))
+
+
+TIMED_ATTN, TIMED_PAGES = 0, 1
+
+
+def sa_set_kernel_events(ctx, which: int, start_event=None, stop_event=None):
+    """Later kernels of kind `which` (TIMED_ATTN, TIMED_PAGES) on ctx are launched
+    bound to these two hipEvent_t handles (ints), which then time the kernel
+    itself; None, None clears."""
+    _check(load_library().sa_set_kernel_events(_ctx_handle(ctx), int(which), start_event or None,
+                                               stop_event or None))
 
 
 def sa_segment_prefill_attn_append(ctx, layout: Layout, layer: int, q, k_pool, v_pool, k_new, v_new, q_len,

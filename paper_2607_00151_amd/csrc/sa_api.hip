@@ -2,6 +2,7 @@
 // planning, plan upload and kernel launches.  Every entry point validates on
 // the host before its first HIP call.
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 
 #include <algorithm>
 #include <cmath>
@@ -84,6 +85,7 @@ struct sa_ctx {
   size_t part_cap = 0;             // bytes
   uint32_t* d_sync = nullptr;      // counters of an attention launch that appends (zero between launches)
   bool exact_scale = false;        // sa_set_exact_scale
+  hipEvent_t kernel_ev[2][2] = {};   // sa_set_kernel_events: [SA_TIMED_ATTN | SA_TIMED_PAGES][start, stop]
 };
 
 namespace {
@@ -192,34 +194,46 @@ bool append_in_attention() {
   return v;
 }
 
-template <int P>
-void launch_attn_p(AttnVariant v, bool pool_rsrc, bool exact, dim3 grid, hipStream_t st, const sa::AttnArgs& a) {
-  if (v.pipe == 1 && exact && pool_rsrc)
-    hipLaunchKernelGGL((sa::attn_pipe_kernel<P, true, false, true>), grid, dim3(256), 0, st, a);
-  else if (v.pipe == 1 && exact)
-    hipLaunchKernelGGL((sa::attn_pipe_kernel<P, false, false, true>), grid, dim3(256), 0, st, a);
-  else if (v.pipe == 2 && pool_rsrc)
-    hipLaunchKernelGGL((sa::attn_pp_kernel<P, true>), grid, dim3(512), 0, st, a);
-  else if (v.pipe == 2)
-    hipLaunchKernelGGL((sa::attn_pp_kernel<P, false>), grid, dim3(512), 0, st, a);
-  else if (v.pipe && a.app_tickets > 0 && pool_rsrc)
-    hipLaunchKernelGGL((sa::attn_pipe_kernel<P, true, true>), grid, dim3(256), 0, st, a);
-  else if (v.pipe && a.app_tickets > 0)
-    hipLaunchKernelGGL((sa::attn_pipe_kernel<P, false, true>), grid, dim3(256), 0, st, a);
-  else if (v.pipe && pool_rsrc)
-    hipLaunchKernelGGL((sa::attn_pipe_kernel<P, true, false>), grid, dim3(256), 0, st, a);
-  else if (v.pipe)
-    hipLaunchKernelGGL((sa::attn_pipe_kernel<P, false, false>), grid, dim3(256), 0, st, a);
+// A kernel launch; with timing events set (sa_set_kernel_events) it goes
+// through hipExtLaunchKernelGGL, which binds both events to the kernel itself,
+// so their elapsed time is the kernel's execution on the device.
+template <typename K, typename A>
+void launch_timed(K kernel, dim3 grid, dim3 block, hipStream_t st, const hipEvent_t* ev, const A& a) {
+  if (ev[0] != nullptr)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, st, ev[0], ev[1], 0, a);
   else
-    hipLaunchKernelGGL((sa::attn_kernel<P, 1, 4>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL(kernel, grid, block, 0, st, a);
+}
+
+template <int P>
+void launch_attn_p(AttnVariant v, bool pool_rsrc, bool exact, dim3 grid, hipStream_t st, const hipEvent_t* ev,
+                   const sa::AttnArgs& a) {
+  if (v.pipe == 1 && exact && pool_rsrc)
+    launch_timed(sa::attn_pipe_kernel<P, true, false, true>, grid, dim3(256), st, ev, a);
+  else if (v.pipe == 1 && exact)
+    launch_timed(sa::attn_pipe_kernel<P, false, false, true>, grid, dim3(256), st, ev, a);
+  else if (v.pipe == 2 && pool_rsrc)
+    launch_timed(sa::attn_pp_kernel<P, true>, grid, dim3(512), st, ev, a);
+  else if (v.pipe == 2)
+    launch_timed(sa::attn_pp_kernel<P, false>, grid, dim3(512), st, ev, a);
+  else if (v.pipe && a.app_tickets > 0 && pool_rsrc)
+    launch_timed(sa::attn_pipe_kernel<P, true, true>, grid, dim3(256), st, ev, a);
+  else if (v.pipe && a.app_tickets > 0)
+    launch_timed(sa::attn_pipe_kernel<P, false, true>, grid, dim3(256), st, ev, a);
+  else if (v.pipe && pool_rsrc)
+    launch_timed(sa::attn_pipe_kernel<P, true, false>, grid, dim3(256), st, ev, a);
+  else if (v.pipe)
+    launch_timed(sa::attn_pipe_kernel<P, false, false>, grid, dim3(256), st, ev, a);
+  else
+    launch_timed(sa::attn_kernel<P, 1, 4>, grid, dim3(256), st, ev, a);
 }
 
 // pool_rsrc: a layer's K (and V) pool spans < 2^31 bytes, so one buffer
 // resource per pool addresses every page with a 32-bit offset
 void launch_attn(int page_size, AttnVariant v, bool pool_rsrc, bool exact, dim3 grid, hipStream_t st,
-                 const sa::AttnArgs& a) {
-  if (page_size == 16) launch_attn_p<16>(v, pool_rsrc, exact, grid, st, a);
-  else launch_attn_p<32>(v, pool_rsrc, exact, grid, st, a);
+                 const hipEvent_t* ev, const sa::AttnArgs& a) {
+  if (page_size == 16) launch_attn_p<16>(v, pool_rsrc, exact, grid, st, ev, a);
+  else launch_attn_p<32>(v, pool_rsrc, exact, grid, st, ev, a);
 }
 
 }  // namespace
@@ -358,7 +372,8 @@ sa_status sa_kv_append(sa_ctx* ctx, const sa_layout* layout, int32_t layer, void
   a.P = layout->page_size;
   const int64_t per_block = 256 * sa::kAppendChunksPerThread;
   const int64_t blocks = (a.total_chunks + per_block - 1) / per_block;
-  hipLaunchKernelGGL(sa::append_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, a);
+  launch_timed(sa::append_kernel, dim3((unsigned)blocks), dim3(256), (hipStream_t)stream,
+               ctx->kernel_ev[SA_TIMED_PAGES], a);
   SA_HIP(hipGetLastError());
   return SA_OK;
 }
@@ -553,8 +568,8 @@ sa_status splice_launch(sa_ctx* ctx, const sa_layout* layout, const void* k_src,
   const int64_t table_blocks = (std::max<int64_t>(n_dst, batch + 1) + sa::kAsmThreads - 1) / sa::kAsmThreads;
   const int64_t gx = std::max<int64_t>(units + a.app_blocks, table_blocks);
   if (gx > 0)
-    hipLaunchKernelGGL(sa::assemble_kernel, dim3((unsigned)gx, (unsigned)layout->num_layers),
-                       dim3(sa::kAsmThreads), 0, (hipStream_t)stream, a);
+    launch_timed(sa::assemble_kernel, dim3((unsigned)gx, (unsigned)layout->num_layers),
+                 dim3(sa::kAsmThreads), (hipStream_t)stream, ctx->kernel_ev[SA_TIMED_PAGES], a);
   SA_HIP(hipGetLastError());
   return SA_OK;
 }
@@ -628,7 +643,8 @@ sa_status sa_kv_splice_alias(sa_ctx* ctx, const sa_layout* layout, int32_t batch
   a.n_dst = (int32_t)sp.n_dst;
   a.B = batch;
   const int64_t blocks = (std::max<int64_t>(sp.n_dst, batch + 1) + 255) / 256;
-  hipLaunchKernelGGL(sa::splice_alias_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, a);
+  launch_timed(sa::splice_alias_kernel, dim3((unsigned)blocks), dim3(256), (hipStream_t)stream,
+               ctx->kernel_ev[SA_TIMED_PAGES], a);
   SA_HIP(hipGetLastError());
   return SA_OK;
 }
@@ -890,7 +906,8 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
     a.app_tickets = (int32_t)tickets;
   }
   const bool pool_rsrc = layer_elems(layout) * 2 < ((int64_t)1 << 31);
-  launch_attn(layout->page_size, var, pool_rsrc, exact, dim3((unsigned)items.size()), (hipStream_t)stream, a);
+  launch_attn(layout->page_size, var, pool_rsrc, exact, dim3((unsigned)items.size()), (hipStream_t)stream,
+              ctx->kernel_ev[SA_TIMED_ATTN], a);
   SA_HIP(hipGetLastError());
   if (!groups.empty()) {
     sa::MergeArgs m{};
@@ -927,6 +944,18 @@ sa_status sa_set_exact_scale(sa_ctx* ctx, int32_t enable) {
   sa_status s = check_ctx(ctx);
   if (s != SA_OK) return s;
   ctx->exact_scale = enable != 0;
+  return SA_OK;
+}
+
+sa_status sa_set_kernel_events(sa_ctx* ctx, int32_t which, void* start_event, void* stop_event) {
+  sa_status s = check_ctx(ctx);
+  if (s != SA_OK) return s;
+  if (which != SA_TIMED_ATTN && which != SA_TIMED_PAGES)
+    return fail(SA_ERR_SHAPE, "sa_set_kernel_events: which = %d (SA_TIMED_ATTN or SA_TIMED_PAGES)", which);
+  if ((start_event == nullptr) != (stop_event == nullptr))
+    return fail(SA_ERR_NULL, "sa_set_kernel_events: give both events or neither");
+  ctx->kernel_ev[which][0] = (hipEvent_t)start_event;
+  ctx->kernel_ev[which][1] = (hipEvent_t)stop_event;
   return SA_OK;
 }
 

@@ -337,6 +337,56 @@ def test_exact_scale_step_c2_full(ctx_exact):
     check_step(ctx_exact, workloads.make("c2"), per_seq_rows=128)
 
 
+def test_attention_kernel_events(ctx):
+    """The timing hook (sa_set_kernel_events) launches the same kernel: same bits,
+    and its two events span a positive time no longer than events around the call."""
+    print("attention kernel events c1", flush=True)
+    w = workloads.make("c1")
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    o1, _ = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    stream = torch.cuda.current_stream()
+    kev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    cev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for e in kev:
+        e.record(stream)
+    torch.cuda.synchronize()
+    sa.sa_set_kernel_events(ctx, sa.TIMED_ATTN, kev[0].cuda_event, kev[1].cuda_event)
+    try:
+        cev[0].record(stream)
+        o2, _ = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+        cev[1].record(stream)
+    finally:
+        sa.sa_set_kernel_events(ctx, sa.TIMED_ATTN)
+    torch.cuda.synchronize()
+    sa.sa_sync_check(ctx)
+    assert torch.equal(o1, o2)
+    k_ms, c_ms = kev[0].elapsed_time(kev[1]), cev[0].elapsed_time(cev[1])
+    print(f"  kernel {k_ms * 1e3:.1f} us, call {c_ms * 1e3:.1f} us")
+    assert 0.0 < k_ms <= c_ms
+    # the page kernels: an append timed by its own events writes the same bits
+    kp2, vp2 = new_pool(w, 1), new_pool(w, 1)
+    indptr, indices = dev_i32(w.pages_indptr), dev_i32(w.pages)
+    pev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for e in pev:
+        e.record(stream)
+    torch.cuda.synchronize()
+    sa.sa_set_kernel_events(ctx, sa.TIMED_PAGES, pev[0].cuda_event, pev[1].cuda_event)
+    try:
+        sa.sa_kv_append(ctx, L, 0, kp2, vp2, dev_u16(w.k_seg()), dev_u16(w.v_seg()), w.pre, w.qlen,
+                        indptr, indices)
+    finally:
+        sa.sa_set_kernel_events(ctx, sa.TIMED_PAGES)
+    torch.cuda.synchronize()
+    sa.sa_sync_check(ctx)
+    assert pev[0].elapsed_time(pev[1]) > 0.0
+    kp3, vp3 = new_pool(w, 1), new_pool(w, 1)
+    sa.sa_kv_append(ctx, L, 0, kp3, vp3, dev_u16(w.k_seg()), dev_u16(w.v_seg()), w.pre, w.qlen,
+                    indptr, indices)
+    sa.sa_sync_check(ctx)
+    assert torch.equal(kp2, kp3) and torch.equal(vp2, vp3)
+
+
 def test_page_permutation_invariance(ctx):
     """Where the pages sit in the pool does not change a single output bit."""
     w = workloads.make("c1")
