@@ -220,12 +220,28 @@ def config_mode(args):
     torch.cuda.synchronize()
     ms_per_step = t0.elapsed_time(t1) / K
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
-    for e in evs:
+    # kernel events bound to the attention kernel and to the first page kernel
+    # of the step (sa_set_kernel_events): their execution on the device
+    kev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    for e in kev:
+        for x in e:
+            x.record(stream)
+    torch.cuda.synchronize()
+    one_page_kernel = not (a is not None and args.fuse == "none")
+    for e, k in zip(evs, kev):
+        sa.sa_set_kernel_events(ctx, sa.TIMED_ATTN, k[0].cuda_event, k[1].cuda_event)
+        if one_page_kernel:
+            sa.sa_set_kernel_events(ctx, sa.TIMED_PAGES, k[2].cuda_event, k[3].cuda_event)
         step(e)
+    sa.sa_set_kernel_events(ctx, sa.TIMED_ATTN)
+    sa.sa_set_kernel_events(ctx, sa.TIMED_PAGES)
     torch.cuda.synchronize()
     sa.sa_sync_check(ctx)
-    first_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    attn_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    first_call_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    first_ms = float(np.mean([k[2].elapsed_time(k[3]) for k in kev])) if one_page_kernel else first_call_ms
+    attn_call_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    attn_kernel_ms = float(np.mean([k[0].elapsed_time(k[1]) for k in kev]))
+    attn_ms = attn_kernel_ms
     flops = w.attn_flops()
     tflops = flops / (attn_ms * 1e-3) / 1e12
     rec = {
@@ -235,8 +251,11 @@ def config_mode(args):
         "config": {"workload": f"{w.name}: batch {w.batch}, Hq {Hq} / Hkv {Hkv} / d 128, page {P}, "
                                f"prefix {int(w.pre.min())}..{int(w.pre.max())}, segment {int(w.qlen.min())}.."
                                f"{int(w.qlen.max())}", "segment_tokens": T, "cached_keys": int(w.kv.sum())},
-        "attn": {"ms": attn_ms, "gflop": flops / 1e9, "tflops": tflops, "frac_of_bf16_peak": tflops / PEAK_BF16_TFLOPS},
-        first_name: {"ms": first_ms, "bytes": first_bytes, "gbs": first_bytes / (first_ms * 1e-3) / 1e9,
+        "attn": {"ms": attn_ms, "timing": "kernel events (the attention kernel; a split launch's merge not "
+                                          "included)", "call_ms": attn_call_ms,
+                 "gflop": flops / 1e9, "tflops": tflops, "frac_of_bf16_peak": tflops / PEAK_BF16_TFLOPS},
+        first_name: {"ms": first_ms, "timing": "kernel events" if one_page_kernel else "call events",
+                     "call_ms": first_call_ms, "bytes": first_bytes, "gbs": first_bytes / (first_ms * 1e-3) / 1e9,
                      "frac_of_hbm": first_bytes / (first_ms * 1e-3) / 1e9 / PEAK_HBM_GBS},
     }
     dec = w.qlen == 1
@@ -248,13 +267,16 @@ def config_mode(args):
             os_ = torch.empty((len(rows), Hq, 128), dtype=torch.int16, device="cuda")
             ql = np.where(sel, w.qlen, 0)
             sub = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+            for x, y in sub:
+                x.record(stream)
+                y.record(stream)
             for i in range(args.warmup + K):
                 if i >= args.warmup:
-                    sub[i - args.warmup][0].record(stream)
+                    x, y = sub[i - args.warmup]
+                    sa.sa_set_kernel_events(ctx, sa.TIMED_ATTN, x.cuda_event, y.cuda_event)
                 sa.sa_segment_prefill_attn(ctx, L, 0, qs, kp, vp, ql, np.where(sel, w.kv, 0), pages[0], pages[1],
                                            w.scale, os_)
-                if i >= args.warmup:
-                    sub[i - args.warmup][1].record(stream)
+            sa.sa_set_kernel_events(ctx, sa.TIMED_ATTN)
             torch.cuda.synchronize()
             sa.sa_sync_check(ctx)
             keys = int(w.kv[sel].sum())
