@@ -284,6 +284,30 @@ def config_mode(args):
                          "cached_keys": keys}
         d = rec["decode_only"]
         d["kv_gbs"] = d["cached_keys"] * Hkv * 128 * 2 * 2 / (d["ms"] * 1e-3) / 1e9
+        # inside the mixed launch: when the decode rows' workgroups end, from the
+        # per-workgroup clock the kernel writes (sa_set_block_clock)
+        buf = torch.full((4 * 65536,), -1, dtype=torch.int64, device="cuda")
+        khz = sa.sa_set_block_clock(ctx, buf)
+        spans, dec_done, pre_done = [], [], []
+        for _ in range(K):
+            buf.fill_(-1)
+            sa.sa_segment_prefill_attn(ctx, L, 0, q, kp, vp, w.qlen, w.kv, pages[0], pages[1], w.scale, o, lse)
+            torch.cuda.synchronize()
+            r = buf.view(-1, 4).cpu().numpy()
+            r = r[(r[:, 0] != -1) & (r[:, 3] != 0)]
+            t0c = r[:, 0].min()
+            to_ms = 1.0 / khz
+            spans.append((r[:, 1].max() - t0c) * to_ms)
+            dec_done.append((r[r[:, 3] == 1, 1].max() - t0c) * to_ms)
+            pre_done.append((r[r[:, 3] > 1, 1].max() - t0c) * to_ms)
+        sa.sa_set_block_clock(ctx, None)
+        sa.sa_sync_check(ctx)
+        rec["mixed_launch_clock"] = {
+            "about": "one launch over decode rows and prefill segments; per-workgroup device clock "
+                     f"({khz} kHz): time from the first workgroup's start",
+            "decode_rows_done_ms": float(np.mean(dec_done)), "prefill_done_ms": float(np.mean(pre_done)),
+            "span_ms": float(np.mean(spans)),
+            "prefill_tokens_per_s": float(int(w.qlen[w.qlen > 1].sum()) / (np.mean(pre_done) * 1e-3))}
     ctx.close()
     print(json.dumps(rec), flush=True)
 

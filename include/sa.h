@@ -288,6 +288,25 @@ sa_status sa_set_exact_scale(sa_ctx *ctx, int32_t enable);
 sa_status sa_set_kernel_events(sa_ctx *ctx, int32_t which, void *start_event, void *stop_event);
 
 /*
+ * sa_set_block_clock — per-workgroup timestamps for measurement (which work of
+ * a mixed decode + prefill launch ends when; paper Sec. 4 and Alg. 2 batch
+ * decode requests with prefill chunks).  While set, each launch of the default
+ * attention kernel writes, for every workgroup w, four uint64 words at
+ * d_buf[4w]: the device's constant-rate wall clock (s_memrealtime) when w
+ * started and when all its output stores were done, its sequence index and
+ * that sequence's q_len (1: a decode row; 0 for a workgroup with no work, which
+ * the planner adds to even out the XCDs).  The launch has one workgroup per
+ * work item, at most max_blocks of them, else it fails with SA_ERR_SHAPE
+ * before launching.  d_buf: device memory of 32 * max_blocks bytes, 8-byte
+ * aligned, owned by the caller; the words of one launch are overwritten by
+ * the next.  clock_khz (nullable, host): receives the clock's rate in kHz.
+ * NULL, 0 clears.  The other attention kernels (SA_ATTN_VARIANT 1, 2) write
+ * nothing.  Errors: SA_ERR_NULL (context), SA_ERR_SHAPE, SA_ERR_ALIGN,
+ * SA_ERR_HIP.
+ */
+sa_status sa_set_block_clock(sa_ctx *ctx, void *d_buf, int64_t max_blocks, int64_t *clock_khz);
+
+/*
  * sa_segment_prefill_attn_append — the segment's append and its attention in
  * one call: each sequence's h_q_len[b] new K/V rows are written to its
  * logical positions h_kv_len[b] - h_q_len[b] .. h_kv_len[b] - 1 (as

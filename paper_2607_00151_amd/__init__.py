@@ -16,7 +16,7 @@ __all__ = [
     "Layout", "Context", "SaError", "library_path", "load_library",
     "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append", "sa_kv_splice_alias",
     "sa_segment_prefill_attn", "sa_segment_prefill_attn_append", "sa_set_exact_scale", "sa_set_kernel_events",
-    "sa_sync_check", "EXPORTED_SYMBOLS",
+    "sa_set_block_clock", "sa_sync_check", "EXPORTED_SYMBOLS",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -26,7 +26,7 @@ _lib = None
 EXPORTED_SYMBOLS = ("sa_create", "sa_destroy", "sa_status_string", "sa_last_error",
                     "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
                     "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append",
-                    "sa_set_exact_scale", "sa_set_kernel_events")
+                    "sa_set_exact_scale", "sa_set_kernel_events", "sa_set_block_clock")
 
 STATUS = {0: "SA_OK", 1: "SA_ERR_NULL", 2: "SA_ERR_SHAPE", 3: "SA_ERR_UNSUPPORTED",
           4: "SA_ERR_ALIGN", 5: "SA_ERR_RANGE", 6: "SA_ERR_NO_PAGES", 7: "SA_ERR_HIP",
@@ -84,9 +84,10 @@ def load_library():
                                                    ctypes.c_float, P, P, P]
     lib.sa_set_exact_scale.argtypes = [P, I32]
     lib.sa_set_kernel_events.argtypes = [P, I32, P, P]
+    lib.sa_set_block_clock.argtypes = [P, P, I64, ctypes.POINTER(ctypes.c_int64)]
     for name in ("sa_create", "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
                  "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append",
-                 "sa_set_exact_scale", "sa_set_kernel_events"):
+                 "sa_set_exact_scale", "sa_set_kernel_events", "sa_set_block_clock"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -258,6 +259,18 @@ def sa_set_exact_scale(ctx, enable: bool = True):
     """Later attention calls on ctx apply the softmax scale to each score in fp32
     (enable) or fold it into the bf16 query rows (the default)."""
     _check(load_library().sa_set_exact_scale(_ctx_handle(ctx), int(bool(enable))))
+
+
+def sa_set_block_clock(ctx, buf=None) -> int:
+    """Later launches of the default attention kernel on ctx write, per workgroup,
+    four int64 words into buf (a device int64 tensor of 4 x max workgroups):
+    start and end clock, sequence, q_len.  Returns the clock's rate in kHz.
+    None clears."""
+    khz = ctypes.c_int64(0)
+    n = 0 if buf is None else buf.numel() // 4
+    _check(load_library().sa_set_block_clock(_ctx_handle(ctx), None if buf is None else _ptr(buf), n,
+                                             ctypes.byref(khz)))
+    return int(khz.value)
 
 
 TIMED_ATTN, TIMED_PAGES = 0, 1

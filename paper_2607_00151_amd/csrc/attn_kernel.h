@@ -88,6 +88,9 @@ struct AttnArgs {
   int64_t app_chunks;       // sum q_len * Hkv * 16: 16-byte chunks of K (and of V)
   int32_t app_tickets;      // 64 ceil(app_chunks / (64 kAppTicket))
   int32_t B;                // sequences in seqs
+  // nullable (attn_pipe_kernel only): per block {start, end} of the device's
+  // constant-rate clock and the item's {sequence, q_len}, four words per block
+  uint64_t* blk_clock;
 };
 
 // Lazy rescaling: the exponent offset only moves when a row's running max

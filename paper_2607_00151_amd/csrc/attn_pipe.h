@@ -834,6 +834,12 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t v_lds0[kTileBytes], v_lds1[kTileBytes];
   if constexpr (kApp) app_produce<P>(a);
   const AttnItem it = ld_uniform(a.items + blockIdx.x);
+  if (a.blk_clock != nullptr && threadIdx.x == 0) {
+    uint64_t* r = a.blk_clock + 4 * (int64_t)blockIdx.x;
+    r[0] = __builtin_amdgcn_s_memrealtime();
+    r[2] = (uint64_t)(uint32_t)it.seq;
+    r[3] = (uint64_t)(uint32_t)it.q_len;
+  }
   if (it.kv_begin < it.kv_end) {                            // else a padding item
     const SeqDesc sd{it.q_start, it.q_len, it.kv_len, 0};
     const PipeLds L{(lds_u8*)k_lds0, (lds_u8*)k_lds1, (lds_u8*)v_lds0, (lds_u8*)v_lds1,
@@ -841,6 +847,11 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
     pipe_group<P, kPoolRsrc, 1, 0, kApp, kExact>(a, it, sd, L);
   }
   if constexpr (kApp) app_finish(a);
+  if (a.blk_clock != nullptr) {
+    // every wave's stores are done once the barrier is passed
+    __syncthreads();
+    if (threadIdx.x == 0) a.blk_clock[4 * (int64_t)blockIdx.x + 1] = __builtin_amdgcn_s_memrealtime();
+  }
 }
 
 // Two groups of four waves per block on the same rows, each over half of the

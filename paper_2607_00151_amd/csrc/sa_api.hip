@@ -86,6 +86,8 @@ struct sa_ctx {
   uint32_t* d_sync = nullptr;      // counters of an attention launch that appends (zero between launches)
   bool exact_scale = false;        // sa_set_exact_scale
   hipEvent_t kernel_ev[2][2] = {};   // sa_set_kernel_events: [SA_TIMED_ATTN | SA_TIMED_PAGES][start, stop]
+  uint64_t* blk_clock = nullptr;     // sa_set_block_clock: device buffer, 4 words per block
+  int64_t blk_clock_cap = 0;         // blocks it holds
 };
 
 namespace {
@@ -905,6 +907,12 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
     if (tickets > INT32_MAX / 2) return fail(SA_ERR_SHAPE, "too many new rows for one launch");
     a.app_tickets = (int32_t)tickets;
   }
+  if (ctx->blk_clock != nullptr && var.pipe == 1) {
+    if ((int64_t)items.size() > ctx->blk_clock_cap)
+      return fail(SA_ERR_SHAPE, "block clock buffer holds %lld blocks, the launch has %zu",
+                  (long long)ctx->blk_clock_cap, items.size());
+    a.blk_clock = ctx->blk_clock;
+  }
   const bool pool_rsrc = layer_elems(layout) * 2 < ((int64_t)1 << 31);
   launch_attn(layout->page_size, var, pool_rsrc, exact, dim3((unsigned)items.size()), (hipStream_t)stream,
               ctx->kernel_ev[SA_TIMED_ATTN], a);
@@ -956,6 +964,23 @@ sa_status sa_set_kernel_events(sa_ctx* ctx, int32_t which, void* start_event, vo
     return fail(SA_ERR_NULL, "sa_set_kernel_events: give both events or neither");
   ctx->kernel_ev[which][0] = (hipEvent_t)start_event;
   ctx->kernel_ev[which][1] = (hipEvent_t)stop_event;
+  return SA_OK;
+}
+
+sa_status sa_set_block_clock(sa_ctx* ctx, void* d_buf, int64_t max_blocks, int64_t* clock_khz) {
+  sa_status s = check_ctx(ctx);
+  if (s != SA_OK) return s;
+  if ((d_buf == nullptr) != (max_blocks == 0) || max_blocks < 0)
+    return fail(SA_ERR_SHAPE, "sa_set_block_clock: a buffer needs max_blocks > 0, none needs 0");
+  if (d_buf != nullptr && (reinterpret_cast<uintptr_t>(d_buf) & 7u) != 0)
+    return fail(SA_ERR_ALIGN, "sa_set_block_clock: buffer not 8-byte aligned");
+  if (clock_khz != nullptr) {
+    int khz = 0;
+    SA_HIP(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, ctx->device));
+    *clock_khz = khz;
+  }
+  ctx->blk_clock = (uint64_t*)d_buf;
+  ctx->blk_clock_cap = max_blocks;
   return SA_OK;
 }
 

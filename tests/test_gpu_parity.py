@@ -670,6 +670,44 @@ def test_random_mixed_attention(ctx, k):
     check_lse(w, lse.cpu().numpy(), ref_lse)
 
 
+def test_block_clock_records(ctx):
+    """sa_set_block_clock: one record per workgroup, start <= end, the item's sequence and
+    q_len, and the same output bits as without it; decode rows and prefill rows mixed."""
+    w = build("clock", 77, 16, 4, 128, 16, [3000, 1200, 40, 5000], [1, 300, 1, 64])
+    print("block clock: pre [3000, 1200, 40, 5000] q [1, 300, 1, 64]", flush=True)
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    o1, _ = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    buf = torch.full((4 * 4096,), -1, dtype=torch.int64, device="cuda")
+    khz = sa.sa_set_block_clock(ctx, buf)
+    try:
+        o2, _ = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    finally:
+        sa.sa_set_block_clock(ctx, None)
+    torch.cuda.synchronize()
+    sa.sa_sync_check(ctx)
+    assert torch.equal(o1, o2)
+    assert khz > 0
+    rec = buf.view(-1, 4).cpu().numpy()
+    n = int((rec[:, 0] != -1).sum())
+    assert n > 0 and (rec[n:] == -1).all()          # one record per workgroup, nothing beyond
+    rec = rec[:n]
+    assert (rec[:, 1] >= rec[:, 0]).all()
+    rec = rec[rec[:, 3] != 0]                        # workgroups of padding items report q_len 0
+    assert set(rec[:, 2].tolist()) == set(range(w.batch))
+    assert np.array_equal(rec[:, 3], w.qlen[rec[:, 2]])
+    span_us = (rec[:, 1].max() - rec[:, 0].min()) / khz * 1e3
+    print(f"  {n} workgroups, clock {khz} kHz, span {span_us:.1f} us", flush=True)
+    # a buffer too small for the launch is refused before anything runs
+    small_buf = torch.zeros(4, dtype=torch.int64, device="cuda")
+    sa.sa_set_block_clock(ctx, small_buf)
+    try:
+        with pytest.raises(sa.SaError):
+            attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    finally:
+        sa.sa_set_block_clock(ctx, None)
+
+
 @pytest.mark.timeout(600)
 def test_step_c2_full(ctx):
     print("c2 full step", flush=True)
