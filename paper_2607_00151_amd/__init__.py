@@ -267,6 +267,8 @@ def sa_set_block_clock(ctx, buf=None) -> int:
     start and end clock, sequence, q_len.  Returns the clock's rate in kHz.
     None clears."""
     khz = ctypes.c_int64(0)
+    if buf is not None and (not hasattr(buf, "element_size") or buf.element_size() != 8 or not buf.is_cuda):
+        raise ValueError("sa_set_block_clock needs a device tensor of 8-byte elements")
     n = 0 if buf is None else buf.numel() // 4
     _check(load_library().sa_set_block_clock(_ctx_handle(ctx), None if buf is None else _ptr(buf), n,
                                              ctypes.byref(khz)))
