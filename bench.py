@@ -54,6 +54,8 @@ def parse():
     p.add_argument("--exact-scale", action="store_true",
                    help="apply the softmax scale to each score in fp32 (sa_set_exact_scale)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-xcd-weights", action="store_true",
+                   help="skip measuring the XCDs' speeds and weighing the attention planner by them")
     p.add_argument("--no-gemm-reference", action="store_true",
                    help="skip timing torch's bf16 GEMM (context for the MFMA roofline)")
     p.add_argument("--cpu-stride", type=int, default=1, help="oracle sample: every n-th token")
@@ -401,6 +403,29 @@ def main():
         step(i)
     sa.sa_sync_check(ctx)
     torch.cuda.synchronize()
+    xcd_speed = None
+    if not args.no_xcd_weights:
+        # this GPU's XCD speeds: every XCD runs the same work in this launch (one
+        # KV head each), so each one's mean workgroup time over a few launches
+        # is inversely proportional to its speed (sa_set_block_clock); the
+        # planner then weighs the XCDs by them (sa_set_xcd_weights)
+        cbuf = torch.full((4 * 8192,), -1, dtype=torch.int64, device="cuda")
+        sa.sa_set_block_clock(ctx, cbuf)
+        acc = np.zeros(8)
+        for i in range(5):
+            cbuf.fill_(-1)
+            step(args.warmup + i)
+            torch.cuda.synchronize()
+            r = cbuf.view(-1, 4).cpu().numpy()
+            ids = np.nonzero(r[:, 0] != -1)[0]
+            acc += [float(np.mean(r[ids[ids % 8 == x], 1] - r[ids[ids % 8 == x], 0])) for x in range(8)]
+        sa.sa_set_block_clock(ctx, None)
+        xcd_speed = acc.mean() / acc
+        sa.sa_set_xcd_weights(ctx, xcd_speed)
+        for i in range(20):
+            step(args.warmup + 5 + i)
+        sa.sa_sync_check(ctx)
+        torch.cuda.synchronize()
 
     # The timed region: K whole steps, bracketed by two events and nothing in
     # between.  Per-kernel times come from a second pass of K steps with an
@@ -527,6 +552,39 @@ def main():
         rec["assemble"] = {"ms": asm_ms, "bytes": asm_bytes, "gbs": asm_bytes / (asm_ms * 1e-3) / 1e9,
                            "frac_of_hbm": asm_bytes / (asm_ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
         rec["append"] = {"ms": app_ms, "bytes": app_bytes, "gbs": app_bytes / (app_ms * 1e-3) / 1e9}
+
+    # where the attention launch's time goes across the chip: each workgroup's
+    # start and end on the device clock (sa_set_block_clock), over 10 launches;
+    # workgroup i runs on XCD i % 8
+    buf = torch.full((4 * 8192,), -1, dtype=torch.int64, device="cuda")
+    khz = sa.sa_set_block_clock(ctx, buf)
+    spans, xcd_end, xcd_start, xcd_wg, busy = [], [], [], [], []
+    for i in range(10):
+        buf.fill_(-1)
+        step(args.warmup + 2 * K + i)
+        torch.cuda.synchronize()
+        r = buf.view(-1, 4).cpu().numpy()
+        ids = np.nonzero(r[:, 0] != -1)[0]
+        r = r[ids]
+        t0c, t1c = r[:, 0].min(), r[:, 1].max()
+        us = 1e3 / khz
+        spans.append((t1c - t0c) * us)
+        xcd_end.append([(r[ids % 8 == x, 1].max() - t0c) * us for x in range(8)])
+        xcd_start.append([(r[ids % 8 == x, 0].max() - t0c) * us for x in range(8)])
+        xcd_wg.append([float(np.mean(r[ids % 8 == x, 1] - r[ids % 8 == x, 0])) * us for x in range(8)])
+        busy.append(float((r[:, 1] - r[:, 0]).sum()) / (2 * 256 * (t1c - t0c)))
+    sa.sa_set_block_clock(ctx, None)
+    sa.sa_sync_check(ctx)
+    xe = np.mean(np.array(xcd_end), axis=0)
+    rec["attn"]["xcd_speeds"] = None if xcd_speed is None else [round(float(x), 4) for x in xcd_speed]
+    rec["attn"]["workgroup_clock"] = {
+        "about": "device clock per workgroup, mean of 10 launches: launch span; per XCD when its last "
+                 "workgroup ended, when its last one started, its mean workgroup time; and the share of "
+                 "the 512 workgroup slots' time spent in a workgroup",
+        "span_us": float(np.mean(spans)), "xcd_last_end_us": [round(float(x), 1) for x in xe],
+        "xcd_last_start_us": [round(float(x), 1) for x in np.mean(np.array(xcd_start), axis=0)],
+        "xcd_mean_workgroup_us": [round(float(x), 1) for x in np.mean(np.array(xcd_wg), axis=0)],
+        "slot_busy_frac": float(np.mean(busy))}
 
     if args.assemble_layers > 0:
         # the commit splice of every layer of the model in one launch: the same

@@ -307,6 +307,23 @@ sa_status sa_set_kernel_events(sa_ctx *ctx, int32_t which, void *start_event, vo
 sa_status sa_set_block_clock(sa_ctx *ctx, void *d_buf, int64_t max_blocks, int64_t *clock_khz);
 
 /*
+ * sa_set_xcd_weights — relative speeds of the chip's 8 XCDs (workgroup i of a
+ * launch runs on XCD i % 8) for the attention planner.  The XCDs of one
+ * MI355X do not run equally fast under a long MFMA-bound launch (their clocks
+ * differ by several percent), and a launch ends with its slowest XCD.  With
+ * speeds set, the planner, when it places the work items of each KV head on
+ * one XCD, then swaps longer items of the XCD with the highest load / speed
+ * for shorter items of the one with the lowest until that no longer lowers
+ * the higher of the two; every XCD keeps its number of items.  Results are
+ * unchanged bit for bit (a work item's arithmetic does not depend on where it
+ * runs).  h_speed: host float[8], each finite and > 0 (only ratios matter),
+ * e.g. the inverse of each XCD's mean workgroup time from sa_set_block_clock
+ * on a launch with equal work per XCD; NULL resets to equal speeds.
+ * Errors: SA_ERR_NULL (context), SA_ERR_SHAPE.
+ */
+sa_status sa_set_xcd_weights(sa_ctx *ctx, const float *h_speed);
+
+/*
  * sa_segment_prefill_attn_append — the segment's append and its attention in
  * one call: each sequence's h_q_len[b] new K/V rows are written to its
  * logical positions h_kv_len[b] - h_q_len[b] .. h_kv_len[b] - 1 (as

@@ -16,7 +16,7 @@ __all__ = [
     "Layout", "Context", "SaError", "library_path", "load_library",
     "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append", "sa_kv_splice_alias",
     "sa_segment_prefill_attn", "sa_segment_prefill_attn_append", "sa_set_exact_scale", "sa_set_kernel_events",
-    "sa_set_block_clock", "sa_sync_check", "EXPORTED_SYMBOLS",
+    "sa_set_block_clock", "sa_set_xcd_weights", "sa_sync_check", "EXPORTED_SYMBOLS",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -26,7 +26,8 @@ _lib = None
 EXPORTED_SYMBOLS = ("sa_create", "sa_destroy", "sa_status_string", "sa_last_error",
                     "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
                     "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append",
-                    "sa_set_exact_scale", "sa_set_kernel_events", "sa_set_block_clock")
+                    "sa_set_exact_scale", "sa_set_kernel_events", "sa_set_block_clock",
+                    "sa_set_xcd_weights")
 
 STATUS = {0: "SA_OK", 1: "SA_ERR_NULL", 2: "SA_ERR_SHAPE", 3: "SA_ERR_UNSUPPORTED",
           4: "SA_ERR_ALIGN", 5: "SA_ERR_RANGE", 6: "SA_ERR_NO_PAGES", 7: "SA_ERR_HIP",
@@ -85,9 +86,10 @@ def load_library():
     lib.sa_set_exact_scale.argtypes = [P, I32]
     lib.sa_set_kernel_events.argtypes = [P, I32, P, P]
     lib.sa_set_block_clock.argtypes = [P, P, I64, ctypes.POINTER(ctypes.c_int64)]
+    lib.sa_set_xcd_weights.argtypes = [P, P]
     for name in ("sa_create", "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
                  "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append",
-                 "sa_set_exact_scale", "sa_set_kernel_events", "sa_set_block_clock"):
+                 "sa_set_exact_scale", "sa_set_kernel_events", "sa_set_block_clock", "sa_set_xcd_weights"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -273,6 +275,17 @@ def sa_set_block_clock(ctx, buf=None) -> int:
     _check(load_library().sa_set_block_clock(_ctx_handle(ctx), None if buf is None else _ptr(buf), n,
                                              ctypes.byref(khz)))
     return int(khz.value)
+
+
+def sa_set_xcd_weights(ctx, speeds=None):
+    """Relative speeds of the 8 XCDs for the attention planner (None: equal)."""
+    if speeds is None:
+        _check(load_library().sa_set_xcd_weights(_ctx_handle(ctx), None))
+        return
+    w = np.ascontiguousarray(speeds, dtype=np.float32)
+    if w.shape != (8,):
+        raise ValueError("sa_set_xcd_weights needs 8 speeds")
+    _check(load_library().sa_set_xcd_weights(_ctx_handle(ctx), w.ctypes.data))
 
 
 TIMED_ATTN, TIMED_PAGES = 0, 1

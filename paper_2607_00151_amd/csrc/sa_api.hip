@@ -87,6 +87,8 @@ struct sa_ctx {
   bool exact_scale = false;        // sa_set_exact_scale
   hipEvent_t kernel_ev[2][2] = {};   // sa_set_kernel_events: [SA_TIMED_ATTN | SA_TIMED_PAGES][start, stop]
   uint64_t* blk_clock = nullptr;     // sa_set_block_clock: device buffer, 4 words per block
+  float xcd_weight[8] = {1, 1, 1, 1, 1, 1, 1, 1};   // sa_set_xcd_weights: relative XCD speeds
+  bool xcd_weighted = false;
   int64_t blk_clock_cap = 0;         // blocks it holds
 };
 
@@ -661,6 +663,47 @@ namespace {
 // new K/V rows (k_new, v_new) to its positions kv_len - q_len .. kv_len - 1:
 // as an append launch before the attention, or inside the attention launch
 // (append_in_attention()).
+int64_t item_tiles(const sa::AttnItem& it) { return (it.kv_end - it.kv_begin + sa::kKT - 1) / sa::kKT; }
+
+// The XCDs of one chip do not run equally fast under this load (measured:
+// the slowest one's workgroups take ~7% longer than the fastest one's on the
+// same work, whichever KV head it serves), and the launch ends with the
+// slowest.  Given relative speeds, move work from the XCD with the highest
+// load / speed to the one with the lowest by swapping a longer item of the
+// first for a shorter item of the second: every XCD keeps its number of
+// items, so the launch keeps its rounds; the swapped items read their K/V
+// from another XCD's KV head's L2 less often, which the balance pays for.
+void weigh_xcds(std::vector<std::vector<sa::AttnItem>>& queue, int64_t* load, const float* speed) {
+  for (int iter = 0; iter < 4096; ++iter) {
+    int s = 0, f = 0;
+    for (int x = 1; x < kNumXcd; ++x) {
+      if (load[x] / speed[x] > load[s] / speed[s]) s = x;
+      if (load[x] / speed[x] < load[f] / speed[f]) f = x;
+    }
+    if (s == f || queue[s].empty() || queue[f].empty()) return;
+    size_t a = 0, b = 0;
+    for (size_t i = 1; i < queue[s].size(); ++i)
+      if (item_tiles(queue[s][i]) > item_tiles(queue[s][a])) a = i;
+    for (size_t i = 1; i < queue[f].size(); ++i)
+      if (item_tiles(queue[f][i]) < item_tiles(queue[f][b])) b = i;
+    const int64_t d = item_tiles(queue[s][a]) - item_tiles(queue[f][b]);
+    if (d <= 0) return;
+    // only a swap that lowers the larger of the two costs
+    const double before = load[s] / speed[s];
+    const double after = std::max((load[s] - d) / speed[s], (load[f] + d) / speed[f]);
+    if (after >= before) return;
+    std::swap(queue[s][a], queue[f][b]);
+    load[s] -= d;
+    load[f] += d;
+  }
+}
+
+// Longest first within each XCD's queue (the swaps above mix the order).
+void sort_longest_first(std::vector<sa::AttnItem>& q) {
+  std::stable_sort(q.begin(), q.end(),
+                   [](const sa::AttnItem& x, const sa::AttnItem& y) { return item_tiles(x) > item_tiles(y); });
+}
+
 sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const void* q,
                       const void* k_pool, const void* v_pool, bool append, const void* k_new,
                       const void* v_new, int32_t batch, const int32_t* h_q_len, const int32_t* h_kv_len,
@@ -819,6 +862,10 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
   if (mx > 0 && (double)(mx - mn) <= 0.1 * (double)mx) {
     std::vector<std::vector<sa::AttnItem>> queue(kNumXcd);
     for (const Work& w : work) queue[w.xcd].push_back(w.it);
+    if (ctx->xcd_weighted) {
+      weigh_xcds(queue, load, ctx->xcd_weight);
+      for (auto& qd : queue) sort_longest_first(qd);
+    }
     for (auto& qd : queue) pair_rounds(qd, (size_t)std::max(1, ctx->num_cu / kNumXcd));
     size_t depth = 0;
     for (auto& qd : queue) depth = std::max(depth, qd.size());
@@ -964,6 +1011,22 @@ sa_status sa_set_kernel_events(sa_ctx* ctx, int32_t which, void* start_event, vo
     return fail(SA_ERR_NULL, "sa_set_kernel_events: give both events or neither");
   ctx->kernel_ev[which][0] = (hipEvent_t)start_event;
   ctx->kernel_ev[which][1] = (hipEvent_t)stop_event;
+  return SA_OK;
+}
+
+sa_status sa_set_xcd_weights(sa_ctx* ctx, const float* h_speed) {
+  sa_status s = check_ctx(ctx);
+  if (s != SA_OK) return s;
+  if (h_speed == nullptr) {
+    ctx->xcd_weighted = false;
+    for (float& w : ctx->xcd_weight) w = 1.f;
+    return SA_OK;
+  }
+  for (int x = 0; x < kNumXcd; ++x)
+    if (!(h_speed[x] > 0.f) || !std::isfinite(h_speed[x]))
+      return fail(SA_ERR_SHAPE, "sa_set_xcd_weights: speed[%d] = %g (must be finite and > 0)", x, h_speed[x]);
+  for (int x = 0; x < kNumXcd; ++x) ctx->xcd_weight[x] = h_speed[x];
+  ctx->xcd_weighted = true;
   return SA_OK;
 }
 

@@ -87,6 +87,11 @@ def test_exact_scale_needs_a_context(lib):
     assert b"context" in lib.sa_last_error()
 
 
+def test_xcd_weights_need_a_context(lib):
+    assert lib.sa_set_xcd_weights(None, None) == 1
+    assert b"context" in lib.sa_last_error()
+
+
 def test_block_clock_needs_a_context(lib):
     assert lib.sa_set_block_clock(None, None, 0, None) == 1
     assert b"context" in lib.sa_last_error()

@@ -708,6 +708,45 @@ def test_block_clock_records(ctx):
         sa.sa_set_block_clock(ctx, None)
 
 
+def test_xcd_weights_move_work_not_results(ctx):
+    """sa_set_xcd_weights re-places work items across the XCDs: the output is the same bit
+    for bit (and matches the oracle on sampled rows), and the slow XCD gets fewer key tiles."""
+    w = build("xcdw", 31, 32, 8, 128, 16, [2000], [1024])
+    print("xcd weights: Hq 32 / Hkv 8, pre 2000, q 1024", flush=True)
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    buf = torch.full((4 * 4096,), -1, dtype=torch.int64, device="cuda")
+
+    def run():
+        sa.sa_set_block_clock(ctx, buf)
+        try:
+            o, lse = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+        finally:
+            sa.sa_set_block_clock(ctx, None)
+        torch.cuda.synchronize()
+        return o, lse, buf.view(-1, 4).cpu().numpy().copy()
+
+    o1, lse1, r1 = run()
+    sa.sa_set_xcd_weights(ctx, [1, 1, 1, 1, 1, 1, 1, 0.8])
+    try:
+        o2, lse2, r2 = run()
+    finally:
+        sa.sa_set_xcd_weights(ctx, None)
+    sa.sa_sync_check(ctx)
+    assert torch.equal(o1, o2) and torch.equal(lse1, lse2)
+    n = int((r1[:, 0] != -1).sum())
+    assert n == int((r2[:, 0] != -1).sum()) and n % 8 == 0
+    # XCD 7 (workgroups i % 8 == 7) spends less time on its items than before
+    t1 = (r1[:n, 1] - r1[:n, 0])[7::8].sum()
+    t2 = (r2[:n, 1] - r2[:n, 0])[7::8].sum()
+    print(f"  XCD 7 workgroup time {t1} -> {t2} clock ticks", flush=True)
+    assert t2 < t1
+    toks, heads = sample_rows(w, 64)
+    ref, ref_lse, _ = oracle.attention_rows(w.q, w.k, w.v, w.q_indptr, w.kv_indptr,
+                                            w.num_q_heads, w.num_kv_heads, w.scale, toks, heads)
+    compare(host_u16(o2)[toks, heads], ref, MAX_TOL, MEAN_TOL)
+
+
 @pytest.mark.timeout(600)
 def test_step_c2_full(ctx):
     print("c2 full step", flush=True)
