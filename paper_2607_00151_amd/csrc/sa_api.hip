@@ -665,43 +665,63 @@ namespace {
 // (append_in_attention()).
 int64_t item_tiles(const sa::AttnItem& it) { return (it.kv_end - it.kv_begin + sa::kKT - 1) / sa::kKT; }
 
-// The XCDs of one chip do not run equally fast under this load (measured:
-// the slowest one's workgroups take ~7% longer than the fastest one's on the
-// same work, whichever KV head it serves), and the launch ends with the
-// slowest.  Given relative speeds, move work from the XCD with the highest
-// load / speed to the one with the lowest by swapping a longer item of the
-// first for a shorter item of the second: every XCD keeps its number of
-// items, so the launch keeps its rounds; the swapped items read their K/V
-// from another XCD's KV head's L2 less often, which the balance pays for.
-void weigh_xcds(std::vector<std::vector<sa::AttnItem>>& queue, int64_t* load, const float* speed) {
-  for (int iter = 0; iter < 4096; ++iter) {
-    int s = 0, f = 0;
-    for (int x = 1; x < kNumXcd; ++x) {
-      if (load[x] / speed[x] > load[s] / speed[s]) s = x;
-      if (load[x] / speed[x] < load[f] / speed[f]) f = x;
-    }
-    if (s == f || queue[s].empty() || queue[f].empty()) return;
-    size_t a = 0, b = 0;
-    for (size_t i = 1; i < queue[s].size(); ++i)
-      if (item_tiles(queue[s][i]) > item_tiles(queue[s][a])) a = i;
-    for (size_t i = 1; i < queue[f].size(); ++i)
-      if (item_tiles(queue[f][i]) < item_tiles(queue[f][b])) b = i;
-    const int64_t d = item_tiles(queue[s][a]) - item_tiles(queue[f][b]);
-    if (d <= 0) return;
-    // only a swap that lowers the larger of the two costs
-    const double before = load[s] / speed[s];
-    const double after = std::max((load[s] - d) / speed[s], (load[f] + d) / speed[f]);
-    if (after >= before) return;
-    std::swap(queue[s][a], queue[f][b]);
-    load[s] -= d;
-    load[f] += d;
-  }
-}
-
-// Longest first within each XCD's queue (the swaps above mix the order).
+// Longest first within each XCD's queue.
 void sort_longest_first(std::vector<sa::AttnItem>& q) {
   std::stable_sort(q.begin(), q.end(),
                    [](const sa::AttnItem& x, const sa::AttnItem& y) { return item_tiles(x) > item_tiles(y); });
+}
+
+// Key tiles of the most loaded CU of an XCD whose queue q is sorted longest
+// first and runs in at most two rounds of `round` blocks, the second reversed
+// (block k and block round + k share a CU): q[k] + q[n - 1 - k].
+int64_t busiest_cu(const std::vector<sa::AttnItem>& q, size_t round) {
+  const size_t n = q.size();
+  int64_t m = 0;
+  for (size_t k = 0; k < std::min(n, round); ++k)
+    m = std::max<int64_t>(m, item_tiles(q[k]) + (k + round < n ? item_tiles(q[n - 1 - k]) : 0));
+  return m;
+}
+
+// The XCDs of one chip do not run equally fast under this load (measured:
+// the slowest one's workgroups take ~5-7% longer than the fastest one's on
+// the same work, whichever KV head it serves), and the launch ends with the
+// slowest.  Given relative speeds, move work from the XCD whose busiest CU
+// has the most key tiles per unit of speed to the one with the fewest, by
+// swapping the longest item of the first for the shortest of the second
+// while neither ends above the first's present cost: every XCD keeps its number of
+// items, so the launch keeps its rounds; the items that move read another
+// KV head's K/V than their XCD's others, which the balance pays for.
+// Queues come back sorted longest first.
+void weigh_xcds(std::vector<std::vector<sa::AttnItem>>& queue, size_t round, const float* speed) {
+  for (auto& q : queue) sort_longest_first(q);
+  for (const auto& q : queue)
+    if (q.size() > 2 * round) return;                       // more than two rounds: not handled
+  double cost[kNumXcd];
+  for (int x = 0; x < kNumXcd; ++x) cost[x] = busiest_cu(queue[x], round) / speed[x];
+  for (int iter = 0; iter < 4096; ++iter) {
+    int s = 0, f = 0;
+    for (int x = 1; x < kNumXcd; ++x) {
+      if (cost[x] > cost[s]) s = x;
+      if (cost[x] < cost[f]) f = x;
+    }
+    if (s == f || queue[s].empty() || queue[f].empty()) return;
+    auto& qs = queue[s];
+    auto& qf = queue[f];
+    if (item_tiles(qs.front()) <= item_tiles(qf.back())) return;
+    std::vector<sa::AttnItem> ns = qs, nf = qf;
+    std::swap(ns.front(), nf.back());
+    sort_longest_first(ns);
+    sort_longest_first(nf);
+    // a swap may leave s's busiest CU where it was (another CU of s carries as
+    // much): it is taken as long as neither XCD ends above s's present cost,
+    // since it lowers s's total and the next swaps then lower that CU
+    const double cs = busiest_cu(ns, round) / speed[s], cf = busiest_cu(nf, round) / speed[f];
+    if (cs > cost[s] || cf >= cost[s]) return;
+    qs.swap(ns);
+    qf.swap(nf);
+    cost[s] = cs;
+    cost[f] = cf;
+  }
 }
 
 sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const void* q,
@@ -862,10 +882,7 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
   if (mx > 0 && (double)(mx - mn) <= 0.1 * (double)mx) {
     std::vector<std::vector<sa::AttnItem>> queue(kNumXcd);
     for (const Work& w : work) queue[w.xcd].push_back(w.it);
-    if (ctx->xcd_weighted) {
-      weigh_xcds(queue, load, ctx->xcd_weight);
-      for (auto& qd : queue) sort_longest_first(qd);
-    }
+    if (ctx->xcd_weighted) weigh_xcds(queue, (size_t)std::max(1, ctx->num_cu / kNumXcd), ctx->xcd_weight);
     for (auto& qd : queue) pair_rounds(qd, (size_t)std::max(1, ctx->num_cu / kNumXcd));
     size_t depth = 0;
     for (auto& qd : queue) depth = std::max(depth, qd.size());
