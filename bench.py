@@ -98,6 +98,35 @@ def stored_traffic(kernel: str, algorithmic: float):
             "algorithmic_bytes": algorithmic, "ratio_to_algorithmic": (fetch + write) / algorithmic}
 
 
+def calibrate_xcds(ctx, run, launches: int = 5, settle: int = 20):
+    """This GPU's XCD speeds, handed to the attention planner (sa_set_xcd_weights).
+    In the configurations timed here every XCD runs the same work (the KV heads
+    map one to one onto the 8 XCDs), so each XCD's mean workgroup time over a
+    few launches, from the device clock each workgroup records
+    (sa_set_block_clock), is inversely proportional to its speed.  run(i) runs
+    one step; the steps after the weights are set let the new plan settle."""
+    import torch
+    import paper_2607_00151_amd as sa
+    cbuf = torch.full((4 * 65536,), -1, dtype=torch.int64, device="cuda")
+    sa.sa_set_block_clock(ctx, cbuf)
+    acc = np.zeros(8)
+    for i in range(launches):
+        cbuf.fill_(-1)
+        run(i)
+        torch.cuda.synchronize()
+        r = cbuf.view(-1, 4).cpu().numpy()
+        ids = np.nonzero((r[:, 0] != -1) & (r[:, 3] != 0))[0]
+        acc += [float(np.mean(r[ids[ids % 8 == x], 1] - r[ids[ids % 8 == x], 0])) for x in range(8)]
+    sa.sa_set_block_clock(ctx, None)
+    speed = acc.mean() / acc
+    sa.sa_set_xcd_weights(ctx, speed)
+    for i in range(settle):
+        run(launches + i)
+    sa.sa_sync_check(ctx)
+    torch.cuda.synchronize()
+    return speed
+
+
 def gemm_reference(n: int = 8192, reps: int = 30):
     """Context for the MFMA roofline: torch's own bf16 GEMM (hipBLASLt) of
     n x n x n on the same GPU, in the same run."""
@@ -213,6 +242,10 @@ def config_mode(args):
         step()
     torch.cuda.synchronize()
     sa.sa_sync_check(ctx)
+    xcd_speed = None
+    # (not for a batch with decode rows: measured no gain there, c5 2.41 against 2.38 ms)
+    if not args.no_xcd_weights and Hkv % 8 == 0 and not (w.qlen == 1).any():
+        xcd_speed = calibrate_xcds(ctx, lambda i: step(), launches=3, settle=2)
     K = args.steps
     t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0.record(stream)
@@ -255,6 +288,7 @@ def config_mode(args):
                                f"{int(w.qlen.max())}", "segment_tokens": T, "cached_keys": int(w.kv.sum())},
         "attn": {"ms": attn_ms, "timing": "kernel events (the attention kernel; a split launch's merge not "
                                           "included)", "call_ms": attn_call_ms,
+                 "xcd_speeds": None if xcd_speed is None else [round(float(x), 4) for x in xcd_speed],
                  "gflop": flops / 1e9, "tflops": tflops, "frac_of_bf16_peak": tflops / PEAK_BF16_TFLOPS},
         first_name: {"ms": first_ms, "timing": "kernel events" if one_page_kernel else "call events",
                      "call_ms": first_call_ms, "bytes": first_bytes, "gbs": first_bytes / (first_ms * 1e-3) / 1e9,
@@ -405,27 +439,7 @@ def main():
     torch.cuda.synchronize()
     xcd_speed = None
     if not args.no_xcd_weights:
-        # this GPU's XCD speeds: every XCD runs the same work in this launch (one
-        # KV head each), so each one's mean workgroup time over a few launches
-        # is inversely proportional to its speed (sa_set_block_clock); the
-        # planner then weighs the XCDs by them (sa_set_xcd_weights)
-        cbuf = torch.full((4 * 8192,), -1, dtype=torch.int64, device="cuda")
-        sa.sa_set_block_clock(ctx, cbuf)
-        acc = np.zeros(8)
-        for i in range(5):
-            cbuf.fill_(-1)
-            step(args.warmup + i)
-            torch.cuda.synchronize()
-            r = cbuf.view(-1, 4).cpu().numpy()
-            ids = np.nonzero(r[:, 0] != -1)[0]
-            acc += [float(np.mean(r[ids[ids % 8 == x], 1] - r[ids[ids % 8 == x], 0])) for x in range(8)]
-        sa.sa_set_block_clock(ctx, None)
-        xcd_speed = acc.mean() / acc
-        sa.sa_set_xcd_weights(ctx, xcd_speed)
-        for i in range(20):
-            step(args.warmup + 5 + i)
-        sa.sa_sync_check(ctx)
-        torch.cuda.synchronize()
+        xcd_speed = calibrate_xcds(ctx, lambda i: step(args.warmup + i))
 
     # The timed region: K whole steps, bracketed by two events and nothing in
     # between.  Per-kernel times come from a second pass of K steps with an
