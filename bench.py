@@ -98,13 +98,15 @@ def stored_traffic(kernel: str, algorithmic: float):
             "algorithmic_bytes": algorithmic, "ratio_to_algorithmic": (fetch + write) / algorithmic}
 
 
-def calibrate_xcds(ctx, run, launches: int = 5, settle: int = 20):
+def calibrate_xcds(ctx, run, launches: int = 5, settle: int = 20, refine: int = 2):
     """This GPU's XCD speeds, handed to the attention planner (sa_set_xcd_weights).
     In the configurations timed here every XCD runs the same work (the KV heads
     map one to one onto the 8 XCDs), so each XCD's mean workgroup time over a
     few launches, from the device clock each workgroup records
-    (sa_set_block_clock), is inversely proportional to its speed.  run(i) runs
-    one step; the steps after the weights are set let the new plan settle."""
+    (sa_set_block_clock), is inversely proportional to its speed; `refine`
+    rounds then scale each XCD's speed by how late its last workgroup ends
+    under the weights.  run(i) runs one step; the steps after the weights are
+    set let the new plan settle."""
     import torch
     import paper_2607_00151_amd as sa
     cbuf = torch.full((4 * 65536,), -1, dtype=torch.int64, device="cuda")
@@ -117,11 +119,28 @@ def calibrate_xcds(ctx, run, launches: int = 5, settle: int = 20):
         r = cbuf.view(-1, 4).cpu().numpy()
         ids = np.nonzero((r[:, 0] != -1) & (r[:, 3] != 0))[0]
         acc += [float(np.mean(r[ids[ids % 8 == x], 1] - r[ids[ids % 8 == x], 0])) for x in range(8)]
-    sa.sa_set_block_clock(ctx, None)
     speed = acc.mean() / acc
     sa.sa_set_xcd_weights(ctx, speed)
+    # then correct the estimate on what the weights are for, the time each XCD's
+    # last workgroup ends: an XCD that still ends late gets less speed credit
+    n = launches
+    for _ in range(refine):
+        ends = np.zeros(8)
+        for i in range(launches):
+            cbuf.fill_(-1)
+            run(n)
+            n += 1
+            torch.cuda.synchronize()
+            r = cbuf.view(-1, 4).cpu().numpy()
+            ids = np.nonzero((r[:, 0] != -1) & (r[:, 3] != 0))[0]
+            t0 = r[ids, 0].min()
+            ends += [float(r[ids[ids % 8 == x], 1].max() - t0) for x in range(8)]
+        speed = speed * (ends.mean() / ends)
+        speed = speed / speed.mean()
+        sa.sa_set_xcd_weights(ctx, speed)
+    sa.sa_set_block_clock(ctx, None)
     for i in range(settle):
-        run(launches + i)
+        run(n + i)
     sa.sa_sync_check(ctx)
     torch.cuda.synchronize()
     return speed
