@@ -89,6 +89,9 @@ struct sa_ctx {
   uint64_t* blk_clock = nullptr;     // sa_set_block_clock: device buffer, 4 words per block
   float xcd_weight[8] = {1, 1, 1, 1, 1, 1, 1, 1};   // sa_set_xcd_weights: relative XCD speeds
   bool xcd_weighted = false;
+  // the last weighting's input queues and result: a launch repeating the same
+  // work reuses it instead of searching again
+  std::vector<std::vector<sa::AttnItem>> wq_in, wq_out;
   int64_t blk_clock_cap = 0;         // blocks it holds
 };
 
@@ -908,7 +911,19 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
   if (mx > 0 && (double)(mx - mn) <= 0.1 * (double)mx) {
     std::vector<std::vector<sa::AttnItem>> queue(kNumXcd);
     for (const Work& w : work) queue[w.xcd].push_back(w.it);
-    if (ctx->xcd_weighted) weigh_xcds(queue, (size_t)std::max(1, ctx->num_cu / kNumXcd), ctx->xcd_weight);
+    if (ctx->xcd_weighted) {
+      bool same = ctx->wq_in.size() == queue.size();
+      for (size_t x = 0; same && x < queue.size(); ++x)
+        same = ctx->wq_in[x].size() == queue[x].size() &&
+               memcmp(ctx->wq_in[x].data(), queue[x].data(), queue[x].size() * sizeof(sa::AttnItem)) == 0;
+      if (same) {
+        queue = ctx->wq_out;
+      } else {
+        ctx->wq_in = queue;
+        weigh_xcds(queue, (size_t)std::max(1, ctx->num_cu / kNumXcd), ctx->xcd_weight);
+        ctx->wq_out = queue;
+      }
+    }
     for (auto& qd : queue) pair_rounds(qd, (size_t)std::max(1, ctx->num_cu / kNumXcd));
     size_t depth = 0;
     for (auto& qd : queue) depth = std::max(depth, qd.size());
@@ -1070,6 +1085,8 @@ sa_status sa_set_xcd_weights(sa_ctx* ctx, const float* h_speed) {
       return fail(SA_ERR_SHAPE, "sa_set_xcd_weights: speed[%d] = %g (must be finite and > 0)", x, h_speed[x]);
   for (int x = 0; x < kNumXcd; ++x) ctx->xcd_weight[x] = h_speed[x];
   ctx->xcd_weighted = true;
+  ctx->wq_in.clear();                                      // new speeds: search again
+  ctx->wq_out.clear();
   return SA_OK;
 }
 
