@@ -261,10 +261,10 @@ def config_mode(args):
         step()
     torch.cuda.synchronize()
     sa.sa_sync_check(ctx)
+    # the XCD-speed weights are for launches of at most two rounds of workgroups
+    # (c2); these configurations launch many rounds, which the planner leaves as
+    # placed
     xcd_speed = None
-    # (not for a batch with decode rows: measured no gain there, c5 2.41 against 2.38 ms)
-    if not args.no_xcd_weights and Hkv % 8 == 0 and not (w.qlen == 1).any():
-        xcd_speed = calibrate_xcds(ctx, lambda i: step(), launches=3, settle=2)
     K = args.steps
     t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0.record(stream)

@@ -312,11 +312,11 @@ sa_status sa_set_block_clock(sa_ctx *ctx, void *d_buf, int64_t max_blocks, int64
  * MI355X do not run equally fast under a long MFMA-bound launch (their clocks
  * differ by several percent), and a launch ends with its slowest XCD.  With
  * speeds set, the planner, when it places the work items of each KV head on
- * one XCD, evens out key tiles per unit of speed across the XCDs: for a
- * launch of at most two rounds of workgroups it swaps the longest item of the
- * XCD whose busiest CU is the most loaded for the shortest item of the least
- * loaded one (every XCD keeps its number of items); for more rounds it moves
- * the last items of the most loaded XCD to the least loaded.  Results are
+ * one XCD, evens out key tiles per unit of speed across the XCDs of a launch
+ * of at most two rounds of workgroups: it swaps the longest item of the XCD
+ * whose busiest CU is the most loaded for the shortest item of the least
+ * loaded one (every XCD keeps its number of items).  Launches of more rounds
+ * are placed as without speeds.  Results are
  * unchanged bit for bit (a work item's arithmetic does not depend on where it
  * runs).  h_speed: host float[8], each finite and > 0 (only ratios matter),
  * e.g. the inverse of each XCD's mean workgroup time from sa_set_block_clock

@@ -696,34 +696,12 @@ int64_t busiest_cu(const std::vector<sa::AttnItem>& q, size_t round) {
 // KV head's K/V than their XCD's others, which the balance pays for.
 // Queues of at most two rounds come back sorted longest first.
 void weigh_xcds(std::vector<std::vector<sa::AttnItem>>& queue, size_t round, const float* speed) {
-  bool many_rounds = false;
-  for (const auto& q : queue) many_rounds |= q.size() > 2 * round;
-  if (many_rounds) {
-    // Many rounds: each XCD's CUs take its items as they free, so what counts
-    // is its total.  Move the last (shortest) items of the XCD with the most
-    // key tiles per unit of speed to the end of the one with the fewest while
-    // that lowers the higher of the two; the order of the rest is kept.
-    double tot[kNumXcd];
-    for (int x = 0; x < kNumXcd; ++x) {
-      tot[x] = 0;
-      for (const auto& it : queue[x]) tot[x] += (double)item_tiles(it);
-    }
-    for (int iter = 0; iter < 1 << 16; ++iter) {
-      int s = 0, f = 0;
-      for (int x = 1; x < kNumXcd; ++x) {
-        if (tot[x] / speed[x] > tot[s] / speed[s]) s = x;
-        if (tot[x] / speed[x] < tot[f] / speed[f]) f = x;
-      }
-      if (s == f || queue[s].empty()) return;
-      const double d = (double)item_tiles(queue[s].back());
-      if (std::max((tot[s] - d) / speed[s], (tot[f] + d) / speed[f]) >= tot[s] / speed[s]) return;
-      queue[f].push_back(queue[s].back());
-      queue[s].pop_back();
-      tot[s] -= d;
-      tot[f] += d;
-    }
-    return;
-  }
+  // More than two rounds: each XCD's CUs take its items as they free; moving
+  // the last items of the most loaded XCD to the least loaded one was tried
+  // and measured -1.5% to +1.4% on 16 ragged contexts and on a 64K-key
+  // context, so those launches are left as placed.
+  for (const auto& q : queue)
+    if (q.size() > 2 * round) return;
   for (auto& q : queue) sort_longest_first(q);
   double cost[kNumXcd];
   for (int x = 0; x < kNumXcd; ++x) cost[x] = busiest_cu(queue[x], round) / speed[x];
