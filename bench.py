@@ -36,7 +36,6 @@ import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
-sys.path.insert(0, os.path.join(ROOT, "tests"))
 
 PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA: 256 CU x 4096 flop/clk x 2.4 GHz
 PEAK_HBM_GBS = 8000.0
@@ -51,8 +50,9 @@ def parse():
     p.add_argument("--rotate", type=int, default=8, help="disjoint cache copies cycled per step")
     p.add_argument("--fuse", choices=("attn", "splice", "none"), default="splice",
                    help="which launch carries the append (see the module docstring)")
-    p.add_argument("--exact-scale", action="store_true",
-                   help="apply the softmax scale to each score in fp32 (sa_set_exact_scale)")
+    p.add_argument("--folded-scale", action="store_true",
+                   help="fast mode: fold the softmax scale into the bf16 query rows "
+                        "(sa_set_exact_scale(ctx, 0)); the default applies it to each fp32 score")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-xcd-weights", action="store_true",
                    help="skip measuring the XCDs' speeds and weighing the attention planner by them")
@@ -68,6 +68,41 @@ def parse():
                    help="instead of the step, time a plain device copy of this many bytes "
                         "(calibrates the FETCH_SIZE / WRITE_SIZE counters)")
     return p.parse_args()
+
+
+def dev_u16(a):
+    """uint16 bit patterns -> int16 device tensor (same bits)."""
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()
+
+
+def dev_i32(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(np.asarray(a, dtype=np.int32))).cuda()
+
+
+def new_pool(num_slots, Hkv, P, layers=1):
+    import torch
+    return torch.zeros((layers, num_slots, Hkv, P, 128), dtype=torch.int16, device="cuda")
+
+
+def fill_cache(ctx, L, kp, vp, k_rows, v_rows, lengths, indptr, indices):
+    """Write each sequence's first lengths[b] cache rows (k_rows / v_rows, sequences
+    back to back) at its logical positions 0.. through the page table, with the
+    library's own append kernel (set-up, outside every timed region)."""
+    import paper_2607_00151_amd as sa
+    sa.sa_kv_append(ctx, L, 0, kp, vp, dev_u16(k_rows), dev_u16(v_rows), np.zeros(len(lengths), np.int32),
+                    lengths, indptr, indices)
+    sa.sa_sync_check(ctx)
+
+
+def source_cache(ctx, L, w, kp, vp, src_indices_dev):
+    """The splice's source cache (kept prefix with the dropped pages in place)."""
+    from workloads.configs import source_rows
+    a = w.asm
+    k = np.concatenate([source_rows(w, b, "k") for b in range(w.batch)])
+    v = np.concatenate([source_rows(w, b, "v") for b in range(w.batch)])
+    fill_cache(ctx, L, kp, vp, k, v, a.src_len, dev_i32(a.src_indptr), src_indices_dev)
 
 
 def source_digest() -> str:
@@ -197,7 +232,6 @@ def config_mode(args):
         from paper_2607_00151_amd import build
         build.build()
     import workloads
-    from harness import build_cache, build_source_cache, dev_i32, dev_u16
 
     w = workloads.make(args.config)
     L = sa.Layout(num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads, head_dim=128,
@@ -208,13 +242,15 @@ def config_mode(args):
     o = torch.empty((T, Hq, 128), dtype=torch.int16, device="cuda")
     lse = torch.empty((T, Hq), dtype=torch.float32, device="cuda")
     ctx = sa.Context(0)
-    if args.exact_scale:
-        sa.sa_set_exact_scale(ctx, True)
+    if args.folded_scale:
+        sa.sa_set_exact_scale(ctx, False)
     stream = torch.cuda.current_stream()
     app_bytes = 2 * T * Hkv * 128 * 2 * 2
     a = w.asm
+    kp, vp = new_pool(w.num_slots, Hkv, P), new_pool(w.num_slots, Hkv, P)
     if a is not None:
-        kp, vp, sip, sid, fresh = build_source_cache(w)
+        sip, sid, fresh = dev_i32(a.src_indptr), dev_i32(a.src_indices), dev_i32(a.fresh)
+        source_cache(ctx, L, w, kp, vp, sid)
         dip = torch.zeros(w.batch + 1, dtype=torch.int32, device="cuda")
         did = torch.zeros(len(a.fresh), dtype=torch.int32, device="cuda")
         kept_pages = int(sum(e - b for b, e in a.keep_spans))
@@ -237,7 +273,10 @@ def config_mode(args):
                                                 w.qlen)
         pages = (dip, did)
     else:
-        kp, vp, ip, ix = build_cache(w, with_segment=False)
+        ip, ix = dev_i32(w.pages_indptr), dev_i32(w.pages)
+        pre_k = np.concatenate([w.k[w.prefix_rows(b)] for b in range(w.batch)])
+        pre_v = np.concatenate([w.v[w.prefix_rows(b)] for b in range(w.batch)])
+        fill_cache(ctx, L, kp, vp, pre_k, pre_v, w.pre, ip, ix)
         first_bytes, first_name = app_bytes, "append"
 
         def first():
@@ -386,8 +425,6 @@ def main():
         from paper_2607_00151_amd import build
         build.build()
     import workloads
-    from harness import dev_i32, dev_u16, new_pool, place_range
-    from workloads.configs import source_rows
 
     w = workloads.make("c2")
     a = w.asm
@@ -396,20 +433,17 @@ def main():
     L = sa.Layout(num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads, head_dim=128,
                   page_size=w.page_size, num_layers=1, num_slots=base_slots * R)
 
-    class Big:   # the workload seen through a pool R times larger
-        num_slots = base_slots * R
-        num_kv_heads = w.num_kv_heads
-        page_size = w.page_size
-        head_dim = 128
-    kp, vp = new_pool(Big), new_pool(Big)
+    ctx = sa.Context(0)
+    if args.folded_scale:
+        sa.sa_set_exact_scale(ctx, False)
+    kp, vp = new_pool(base_slots * R, w.num_kv_heads, w.page_size), new_pool(base_slots * R, w.num_kv_heads,
+                                                                              w.page_size)
     copies = []
     for r in range(R):
         off = r * base_slots
-        src_ix = a.src_indices + off
-        for pool, which in ((kp, "k"), (vp, "v")):
-            place_range(pool, 0, w, lambda b, which=which: source_rows(w, b, which), a.src_indptr,
-                        src_ix, a.src_len)
-        copies.append(dict(sip=dev_i32(a.src_indptr), sid=dev_i32(src_ix), fresh=dev_i32(a.fresh + off),
+        sid = dev_i32(a.src_indices + off)
+        source_cache(ctx, L, w, kp, vp, sid)
+        copies.append(dict(sip=dev_i32(a.src_indptr), sid=sid, fresh=dev_i32(a.fresh + off),
                            dip=torch.zeros(w.batch + 1, dtype=torch.int32, device="cuda"),
                            did=torch.zeros(len(a.fresh), dtype=torch.int32, device="cuda")))
     q = dev_u16(w.q)
@@ -417,9 +451,6 @@ def main():
     T = int(w.qlen.sum())
     o = torch.empty((T, w.num_q_heads, 128), dtype=torch.int16, device="cuda")
     lse = torch.empty((T, w.num_q_heads), dtype=torch.float32, device="cuda")
-    ctx = sa.Context(0)
-    if args.exact_scale:
-        sa.sa_set_exact_scale(ctx, True)
     stream = torch.cuda.current_stream()
     fuse = args.fuse
 
@@ -456,9 +487,27 @@ def main():
         step(i)
     sa.sa_sync_check(ctx)
     torch.cuda.synchronize()
+
+    def attn_kernel_pass(n, base):
+        """Mean attention kernel time (kernel events) over n steps."""
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(n)]
+        for e in ev:
+            e[0].record(stream)
+            e[1].record(stream)
+        torch.cuda.synchronize()
+        for i in range(n):
+            sa.sa_set_kernel_events(ctx, sa.TIMED_ATTN, ev[i][0].cuda_event, ev[i][1].cuda_event)
+            step(base + i)
+        sa.sa_set_kernel_events(ctx, sa.TIMED_ATTN)
+        torch.cuda.synchronize()
+        sa.sa_sync_check(ctx)
+        return float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+
+    # the attention kernel as planned without XCD speeds, for comparison
+    unweighted_ms = attn_kernel_pass(args.steps, args.warmup)
     xcd_speed = None
     if not args.no_xcd_weights:
-        xcd_speed = calibrate_xcds(ctx, lambda i: step(args.warmup + i))
+        xcd_speed = calibrate_xcds(ctx, lambda i: step(args.warmup + args.steps + i))
 
     # The timed region: K whole steps, bracketed by two events and nothing in
     # between.  Per-kernel times come from a second pass of K steps with an
@@ -543,12 +592,15 @@ def main():
                         "causal GQA over 8192 + 2048",
             "batch": 1, "prefix": int(w.pre[0]), "segment": T, "page_size": P,
             "cache_copies_rotated": R,
-            "softmax_scale": "per score, fp32" if args.exact_scale else "folded into q (bf16)",
+            "softmax_scale": "folded into q (bf16)" if args.folded_scale else "per score, fp32",
         },
         "attn": {"ms": attn_ms, "timing": "kernel events (hipExtLaunchKernelGGL)", "call_ms": attn_call_ms,
                  "gflop": flops / 1e9, "tflops": attn_tflops,
                  "frac_of_bf16_peak": attn_tflops / PEAK_BF16_TFLOPS,
-                 "tokens_per_s": T / (attn_ms * 1e-3)},
+                 "tokens_per_s": T / (attn_ms * 1e-3),
+                 "without_xcd_weights": {
+                     "ms": unweighted_ms,
+                     "frac_of_bf16_peak": flops / (unweighted_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}},
         "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": attn_tflops / PEAK_BF16_TFLOPS,
                      "traffic": None},

@@ -235,11 +235,11 @@ sa_status sa_kv_splice_alias(sa_ctx *ctx, const sa_layout *layout, int32_t batch
  * rows are bf16 (round to nearest even); `lse` may be NULL.  Sequences with
  * h_q_len[b] == 0 are skipped.  Arithmetic: bf16 MFMA products with fp32
  * accumulation, fp32 online softmax, probabilities rounded to bf16 before the
- * PV product.  By default the kernel multiplies each query row by
- * softmax_scale * log2(e) once and rounds it to bf16, which moves a row's
- * scaled scores by at most 2^-8 * sum_d |scale log2(e) q_d k_d| (log2 units);
- * after sa_set_exact_scale(ctx, 1) it applies the scale to each score in
- * fp32 instead (no such rounding; slower).
+ * PV product.  The scale is applied to each fp32 score (with log2(e)) before
+ * the exponential.  After sa_set_exact_scale(ctx, 0) the kernel instead
+ * multiplies each query row by softmax_scale * log2(e) once and rounds it to
+ * bf16 (faster; moves a row's scaled scores by up to
+ * 2^-8 * sum_d |scale log2(e) q_d k_d| in log2 units).
  *
  * Errors: SA_ERR_SHAPE (0 <= q_len <= kv_len violated, bad batch or layer,
  * softmax_scale not finite and positive),
@@ -253,14 +253,15 @@ sa_status sa_segment_prefill_attn(sa_ctx *ctx, const sa_layout *layout, int32_t 
 
 /*
  * sa_set_exact_scale — how later attention calls on this context apply
- * softmax_scale: enable != 0 multiplies each fp32 score by it (with log2(e))
- * before the exponential; enable == 0 (the default) folds it into the query
- * rows, rounded to bf16 once per row, which saves one fma per score and moves
- * the scores by at most 2^-8 * sum_d |scale log2(e) q_d k_d| -- of the order of
- * the error bf16 query and key rows already carry.  Applies to the default
- * kernel; SA_ATTN_VARIANT=1 always scales in fp32, SA_ATTN_VARIANT=2 never.
- * With exact scaling, sa_segment_prefill_attn_append runs its append as a
- * launch of its own.  Errors: SA_ERR_NULL for a NULL context.
+ * softmax_scale.  enable != 0 (the default) multiplies each fp32 score by it
+ * (with log2(e)) before the exponential: the only roundings are those of the
+ * probabilities to bf16 before the PV product and of the output.  enable == 0
+ * is a fast mode that folds the scale into the query rows, rounded to bf16
+ * once per row, which saves one fma per score and moves the scores by at most
+ * 2^-8 * sum_d |scale log2(e) q_d k_d| (log2 units) -- of the order of the
+ * error bf16 query and key rows already carry, but large when the logits
+ * are.  Applies to the default kernel; SA_ATTN_VARIANT=1 always scales in
+ * fp32, SA_ATTN_VARIANT=2 never.  Errors: SA_ERR_NULL for a NULL context.
  */
 sa_status sa_set_exact_scale(sa_ctx *ctx, int32_t enable);
 

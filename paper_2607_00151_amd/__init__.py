@@ -102,14 +102,43 @@ def _check(status: int):
 
 
 def _ptr(t):
-    """Device (or host) address of a tensor / array, or None."""
+    """Address of a host numpy array, or None."""
     if t is None:
         return None
-    if hasattr(t, "data_ptr"):
-        return t.data_ptr() or None
-    if isinstance(t, int):
-        return t or None
     return t.ctypes.data
+
+
+def _dev(t, what: str, kind: str, min_numel: int = 0, nullable: bool = False):
+    """Device address of a caller tensor after checking what the C ABI will assume
+    of it: a contiguous CUDA tensor whose element type matches `kind` ("i32": int32
+    table entries, "b16": 2-byte bf16 bit patterns, "f32": float32) and that holds at
+    least min_numel elements.  Raises ValueError otherwise; None passes only when
+    nullable."""
+    if t is None:
+        if nullable:
+            return None
+        raise ValueError(f"{what}: a device tensor is required")
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{what}: expected a torch tensor, got {type(t).__name__}")
+    if not t.is_cuda:
+        raise ValueError(f"{what}: tensor is not on a GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{what}: tensor is not contiguous")
+    ok = {"i32": t.dtype == torch.int32,
+          "b16": t.element_size() == 2 and t.dtype != torch.bool,
+          "f32": t.dtype == torch.float32}[kind]
+    if not ok:
+        want = {"i32": "torch.int32", "b16": "a 2-byte dtype (bf16 bits)", "f32": "torch.float32"}[kind]
+        raise ValueError(f"{what}: dtype {t.dtype}, expected {want}")
+    if t.numel() < min_numel:
+        raise ValueError(f"{what}: {t.numel()} elements, at least {min_numel} needed")
+    return t.data_ptr() or None
+
+
+def _pool_numel(layout) -> int:
+    return (int(layout.num_layers) * int(layout.num_slots) * int(layout.num_kv_heads)
+            * int(layout.page_size) * int(layout.head_dim))
 
 
 def _host_i32(x):
@@ -128,8 +157,9 @@ def _stream(stream):
     return int(stream)
 
 
-def _pages(indptr, indices):
-    return _Pages(_ptr(indptr), _ptr(indices))
+def _pages(indptr, indices, batch: int, what: str = "page table"):
+    return _Pages(_dev(indptr, f"{what} indptr", "i32", batch + 1),
+                  _dev(indices, f"{what} indices", "i32", 0))
 
 
 class Context:
@@ -179,29 +209,53 @@ def sa_kv_append(ctx, layout: Layout, layer: int, k_pool, v_pool, k_new, v_new, 
     start, new_len = _host_i32(start), _host_i32(new_len)
     if start.shape != new_len.shape:
         raise ValueError("start and new_len differ in length")
+    B = len(new_len)
+    rows = int(new_len.astype(np.int64).sum()) * int(layout.num_kv_heads) * int(layout.head_dim)
     _check(load_library().sa_kv_append(
-        _ctx_handle(ctx), ctypes.byref(layout), int(layer), _ptr(k_pool), _ptr(v_pool),
-        _ptr(k_new), _ptr(v_new), int(len(new_len)), _ptr(start), _ptr(new_len),
-        _pages(pages_indptr, pages_indices), _stream(stream)))
+        _ctx_handle(ctx), ctypes.byref(layout), int(layer),
+        _dev(k_pool, "k_pool", "b16", _pool_numel(layout)), _dev(v_pool, "v_pool", "b16", _pool_numel(layout)),
+        _dev(k_new, "k_new", "b16", rows, nullable=rows == 0), _dev(v_new, "v_new", "b16", rows, nullable=rows == 0),
+        int(B), _ptr(start), _ptr(new_len), _pages(pages_indptr, pages_indices, B), _stream(stream)))
 
 
-def sa_kv_assemble(ctx, layout: Layout, k_src, v_src, k_dst, v_dst, src_len, keep_indptr,
-                   keep_spans, reserve, src_indptr, src_indices, fresh, dst_indptr, dst_indices,
-                   stream=None):
-    """Returns the kept token count of every sequence (numpy int32)."""
+def _splice_host(layout, src_len, keep_indptr, keep_spans, reserve):
     src_len, reserve = _host_i32(src_len), _host_i32(reserve)
     keep_indptr = _host_i32(keep_indptr)
     keep_spans = _host_i32(np.asarray(keep_spans).reshape(-1))
     B = len(src_len)
     if len(reserve) != B or len(keep_indptr) != B + 1:
         raise ValueError("per-sequence arrays disagree on the batch size")
+    return src_len, keep_indptr, keep_spans, reserve, B
+
+
+def _splice_dev(layout, B, k_src, v_src, k_dst, v_dst, src_indptr, src_indices, fresh, dst_indptr,
+                dst_indices, fresh_nullable=False):
+    n = _pool_numel(layout)
+    return (_dev(k_src, "k_src", "b16", n), _dev(v_src, "v_src", "b16", n),
+            _dev(k_dst, "k_dst", "b16", n), _dev(v_dst, "v_dst", "b16", n),
+            _Pages(_dev(src_indptr, "src indptr", "i32", B + 1),
+                   _dev(src_indices, "src indices", "i32", 0, nullable=True)),
+            _dev(fresh, "fresh", "i32", 0, nullable=fresh_nullable),
+            0 if fresh is None else int(fresh.numel()),
+            _dev(dst_indptr, "dst indptr", "i32", B + 1),
+            _dev(dst_indices, "dst indices", "i32", 0, nullable=True),
+            0 if dst_indices is None else int(dst_indices.numel()))
+
+
+def sa_kv_assemble(ctx, layout: Layout, k_src, v_src, k_dst, v_dst, src_len, keep_indptr,
+                   keep_spans, reserve, src_indptr, src_indices, fresh, dst_indptr, dst_indices,
+                   stream=None):
+    """Returns the kept token count of every sequence (numpy int32)."""
+    src_len, keep_indptr, keep_spans, reserve, B = _splice_host(layout, src_len, keep_indptr, keep_spans,
+                                                                reserve)
+    ks, vs, kd, vd, src, fr, nfr, dip, dix, cap = _splice_dev(layout, B, k_src, v_src, k_dst, v_dst,
+                                                              src_indptr, src_indices, fresh, dst_indptr,
+                                                              dst_indices)
     dst_len = np.zeros(B, dtype=np.int32)
     _check(load_library().sa_kv_assemble(
-        _ctx_handle(ctx), ctypes.byref(layout), _ptr(k_src), _ptr(v_src), _ptr(k_dst), _ptr(v_dst),
-        B, _ptr(src_len), _ptr(keep_indptr), _ptr(keep_spans) if keep_spans.size else None,
-        _ptr(reserve), _pages(src_indptr, src_indices), _ptr(fresh), int(fresh.numel()),
-        _ptr(dst_indptr), _ptr(dst_indices), int(dst_indices.numel()), _ptr(dst_len),
-        _stream(stream)))
+        _ctx_handle(ctx), ctypes.byref(layout), ks, vs, kd, vd, B, _ptr(src_len), _ptr(keep_indptr),
+        _ptr(keep_spans) if keep_spans.size else None, _ptr(reserve), src, fr, nfr, dip, dix, cap,
+        _ptr(dst_len), _stream(stream)))
     return dst_len
 
 
@@ -210,19 +264,21 @@ def sa_kv_assemble_append(ctx, layout: Layout, k_src, v_src, k_dst, v_dst, src_l
                           layer, k_new, v_new, new_len, stream=None):
     """Splice and the segment's append in one launch.  Returns the kept token
     count of every sequence (numpy int32); the new rows follow it."""
-    src_len, reserve, new_len = _host_i32(src_len), _host_i32(reserve), _host_i32(new_len)
-    keep_indptr = _host_i32(keep_indptr)
-    keep_spans = _host_i32(np.asarray(keep_spans).reshape(-1))
-    B = len(src_len)
-    if len(reserve) != B or len(keep_indptr) != B + 1 or len(new_len) != B:
+    src_len, keep_indptr, keep_spans, reserve, B = _splice_host(layout, src_len, keep_indptr, keep_spans,
+                                                                reserve)
+    new_len = _host_i32(new_len)
+    if len(new_len) != B:
         raise ValueError("per-sequence arrays disagree on the batch size")
+    ks, vs, kd, vd, src, fr, nfr, dip, dix, cap = _splice_dev(layout, B, k_src, v_src, k_dst, v_dst,
+                                                              src_indptr, src_indices, fresh, dst_indptr,
+                                                              dst_indices)
+    rows = int(new_len.astype(np.int64).sum()) * int(layout.num_kv_heads) * int(layout.head_dim)
     dst_len = np.zeros(B, dtype=np.int32)
     _check(load_library().sa_kv_assemble_append(
-        _ctx_handle(ctx), ctypes.byref(layout), _ptr(k_src), _ptr(v_src), _ptr(k_dst), _ptr(v_dst),
-        B, _ptr(src_len), _ptr(keep_indptr), _ptr(keep_spans) if keep_spans.size else None,
-        _ptr(reserve), _pages(src_indptr, src_indices), _ptr(fresh), int(fresh.numel()),
-        _ptr(dst_indptr), _ptr(dst_indices), int(dst_indices.numel()), _ptr(dst_len), int(layer),
-        _ptr(k_new), _ptr(v_new), _ptr(new_len), _stream(stream)))
+        _ctx_handle(ctx), ctypes.byref(layout), ks, vs, kd, vd, B, _ptr(src_len), _ptr(keep_indptr),
+        _ptr(keep_spans) if keep_spans.size else None, _ptr(reserve), src, fr, nfr, dip, dix, cap,
+        _ptr(dst_len), int(layer), _dev(k_new, "k_new", "b16", rows, nullable=rows == 0),
+        _dev(v_new, "v_new", "b16", rows, nullable=rows == 0), _ptr(new_len), _stream(stream)))
     return dst_len
 
 
@@ -230,19 +286,25 @@ def sa_kv_splice_alias(ctx, layout: Layout, src_len, keep_indptr, keep_spans, re
                        src_indices, fresh, dst_indptr, dst_indices, stream=None):
     """Zero-copy splice: the destination table shares the surviving source slots.
     Returns the kept token count of every sequence (numpy int32)."""
-    src_len, reserve = _host_i32(src_len), _host_i32(reserve)
-    keep_indptr = _host_i32(keep_indptr)
-    keep_spans = _host_i32(np.asarray(keep_spans).reshape(-1))
-    B = len(src_len)
-    if len(reserve) != B or len(keep_indptr) != B + 1:
-        raise ValueError("per-sequence arrays disagree on the batch size")
+    src_len, keep_indptr, keep_spans, reserve, B = _splice_host(layout, src_len, keep_indptr, keep_spans,
+                                                                reserve)
     dst_len = np.zeros(B, dtype=np.int32)
     _check(load_library().sa_kv_splice_alias(
         _ctx_handle(ctx), ctypes.byref(layout), B, _ptr(src_len), _ptr(keep_indptr),
-        _ptr(keep_spans) if keep_spans.size else None, _ptr(reserve), _pages(src_indptr, src_indices),
-        _ptr(fresh) if fresh is not None else None, int(fresh.numel()) if fresh is not None else 0,
-        _ptr(dst_indptr), _ptr(dst_indices), int(dst_indices.numel()), _ptr(dst_len), _stream(stream)))
+        _ptr(keep_spans) if keep_spans.size else None, _ptr(reserve),
+        _Pages(_dev(src_indptr, "src indptr", "i32", B + 1),
+               _dev(src_indices, "src indices", "i32", 0, nullable=True)),
+        _dev(fresh, "fresh", "i32", 0, nullable=True), 0 if fresh is None else int(fresh.numel()),
+        _dev(dst_indptr, "dst indptr", "i32", B + 1), _dev(dst_indices, "dst indices", "i32", 0, nullable=True),
+        0 if dst_indices is None else int(dst_indices.numel()), _ptr(dst_len), _stream(stream)))
     return dst_len
+
+
+def _attn_dev(layout, q_len, q, o, lse):
+    T = int(q_len.astype(np.int64).sum())
+    n = T * int(layout.num_q_heads) * int(layout.head_dim)
+    return (_dev(q, "q", "b16", n, nullable=T == 0), _dev(o, "o", "b16", n, nullable=T == 0),
+            _dev(lse, "lse", "f32", T * int(layout.num_q_heads), nullable=True), T)
 
 
 def sa_segment_prefill_attn(ctx, layout: Layout, layer: int, q, k_pool, v_pool, q_len, kv_len,
@@ -251,10 +313,12 @@ def sa_segment_prefill_attn(ctx, layout: Layout, layer: int, q, k_pool, v_pool, 
     q_len, kv_len = _host_i32(q_len), _host_i32(kv_len)
     if q_len.shape != kv_len.shape:
         raise ValueError("q_len and kv_len differ in length")
+    qp, op, lp, _ = _attn_dev(layout, q_len, q, o, lse)
+    n = _pool_numel(layout)
     _check(load_library().sa_segment_prefill_attn(
-        _ctx_handle(ctx), ctypes.byref(layout), int(layer), _ptr(q), _ptr(k_pool), _ptr(v_pool),
-        int(len(q_len)), _ptr(q_len), _ptr(kv_len), _pages(pages_indptr, pages_indices),
-        float(softmax_scale), _ptr(o), _ptr(lse), _stream(stream)))
+        _ctx_handle(ctx), ctypes.byref(layout), int(layer), qp, _dev(k_pool, "k_pool", "b16", n),
+        _dev(v_pool, "v_pool", "b16", n), int(len(q_len)), _ptr(q_len), _ptr(kv_len),
+        _pages(pages_indptr, pages_indices, len(q_len)), float(softmax_scale), op, lp, _stream(stream)))
 
 
 def sa_set_exact_scale(ctx, enable: bool = True):
@@ -269,10 +333,11 @@ def sa_set_block_clock(ctx, buf=None) -> int:
     start and end clock, sequence, q_len.  Returns the clock's rate in kHz.
     None clears."""
     khz = ctypes.c_int64(0)
-    if buf is not None and (not hasattr(buf, "element_size") or buf.element_size() != 8 or not buf.is_cuda):
-        raise ValueError("sa_set_block_clock needs a device tensor of 8-byte elements")
+    if buf is not None and (not hasattr(buf, "element_size") or buf.element_size() != 8 or not buf.is_cuda
+                            or not buf.is_contiguous()):
+        raise ValueError("sa_set_block_clock needs a contiguous device tensor of 8-byte elements")
     n = 0 if buf is None else buf.numel() // 4
-    _check(load_library().sa_set_block_clock(_ctx_handle(ctx), None if buf is None else _ptr(buf), n,
+    _check(load_library().sa_set_block_clock(_ctx_handle(ctx), None if buf is None else buf.data_ptr(), n,
                                              ctypes.byref(khz)))
     return int(khz.value)
 
@@ -303,11 +368,15 @@ def sa_segment_prefill_attn_append(ctx, layout: Layout, layer: int, q, k_pool, v
                                    kv_len, pages_indptr, pages_indices, softmax_scale: float, o, lse=None,
                                    stream=None):
     """Writes each sequence's q_len new K/V rows at positions kv_len - q_len .. kv_len - 1,
-    then runs sa_segment_prefill_attn over the result (one launch with the default kernel)."""
+    then runs sa_segment_prefill_attn over the result."""
     q_len, kv_len = _host_i32(q_len), _host_i32(kv_len)
     if q_len.shape != kv_len.shape:
         raise ValueError("q_len and kv_len differ in length")
+    qp, op, lp, T = _attn_dev(layout, q_len, q, o, lse)
+    rows = T * int(layout.num_kv_heads) * int(layout.head_dim)
+    n = _pool_numel(layout)
     _check(load_library().sa_segment_prefill_attn_append(
-        _ctx_handle(ctx), ctypes.byref(layout), int(layer), _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(k_new),
-        _ptr(v_new), int(len(q_len)), _ptr(q_len), _ptr(kv_len), _pages(pages_indptr, pages_indices),
-        float(softmax_scale), _ptr(o), _ptr(lse), _stream(stream)))
+        _ctx_handle(ctx), ctypes.byref(layout), int(layer), qp, _dev(k_pool, "k_pool", "b16", n),
+        _dev(v_pool, "v_pool", "b16", n), _dev(k_new, "k_new", "b16", rows, nullable=T == 0),
+        _dev(v_new, "v_new", "b16", rows, nullable=T == 0), int(len(q_len)), _ptr(q_len), _ptr(kv_len),
+        _pages(pages_indptr, pages_indices, len(q_len)), float(softmax_scale), op, lp, _stream(stream)))

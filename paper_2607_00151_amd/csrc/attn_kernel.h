@@ -93,10 +93,18 @@ struct AttnArgs {
   uint64_t* blk_clock;
 };
 
-// Lazy rescaling: the exponent offset only moves when a row's running max
-// grows by more than this many powers of two, so P stays below 2^kRescaleLog2
-// (bf16 and fp32 hold that easily) and the O rescale is rare.
+// Lazy rescaling (folded-scale mode only): the exponent offset only moves
+// when a row's running max grows by more than this many powers of two, so P
+// stays below 2^kRescaleLog2 (bf16 and fp32 hold that easily) and the O
+// rescale is rare.  Its price is accuracy: a row's largest probability is
+// then 2^x for some x in (0, kRescaleLog2], which bf16 rounds by up to 2^-9
+// of itself, an error that reaches the output undiluted when one key
+// dominates the row.
 constexpr float kRescaleLog2 = 8.0f;
+// The exact-scale kernels move the offset whenever a row's max grows
+// (threshold 0): the largest probability of every row is then exactly 1 in
+// bf16, and the only roundings left on the dominant term are the output's.
+constexpr float kRescaleLog2Exact = 0.0f;
 
 __device__ __forceinline__ int swz_k(int key) { return key & 15; }
 __device__ __forceinline__ int swz_v(int key) { return (key & 3) << 2; }
@@ -322,7 +330,7 @@ __global__ __launch_bounds__(64 * WAVES, (QT == 1 ? 2 : 1)) void attn_kernel(Att
           for (int e = 0; e < 16; ++e) mx = vmax(mx, s[kt][qt][e]);
         mx = pair_max(mx);
         const float cand = mx * a.c;
-        if (__ballot(cand > m_used[qt] + kRescaleLog2)) {
+        if (__ballot(cand > m_used[qt] + kRescaleLog2Exact)) {
           const float m_new = fmaxf(m_used[qt], cand);
           const float alpha = (m_new == -INFINITY) ? 1.f : exp2f_fast(m_used[qt] - m_new);
           m_used[qt] = m_new;

@@ -20,15 +20,16 @@
 // than making all of P(t) in phase 1.  Steps whose next tile needs the causal
 // mask, and the last step, run the same sequence without the interleaving.
 //
-// The exponent x = c s - m (c = softmax scale times log2 e, m the offset in
-// use) comes out of the MFMA itself: the query rows are scaled by c once, when
-// they are loaded, and every S accumulation starts from -m instead of zero.
-// That takes the 32 fma per lane and tile off the VALU.  The price is one
-// more bf16 rounding, of c q: each x moves by at most 2^-8 sum_d |c q_d k_d|,
-// so the log-sum-exp moves by at most ln 2 times that, over the row's keys;
-// at moderate logits the output's own error stays far inside its tolerance.
-// The exact-scale form (kExact) keeps q as given, starts the accumulations
-// from zero and computes each exponent as fma(s, c, -m) in fp32.
+// Two ways to apply the softmax scale.  The default (kExact) keeps q as
+// given, starts the S accumulations from zero and computes each exponent as
+// fma(s, c, -m) in fp32 (c = softmax scale times log2 e, m the row's offset),
+// with the offset moved whenever a row's max grows.  The fast mode folds the
+// scale into the MFMA instead: the query rows are scaled by c once, when they
+// are loaded, and every S accumulation starts from -m, which takes the 32 fma
+// per lane and tile off the VALU; its offset moves only when the max grows by
+// 2^kRescaleLog2.  Its price is one more bf16 rounding, of c q (each x moves
+// by at most 2^-8 sum_d |c q_d k_d|, so the log-sum-exp by at most ln 2 times
+// that), plus the rounding of a row's largest probability.
 #pragma once
 
 #include "attn_kernel.h"
@@ -408,13 +409,14 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
         if (key > lim) S[kt][e] = -INFINITY;
       }
   };
-  // lazy rescale, given the row max mx of a tile's x values: move the offset
-  // when c (row max) outgrows it by 2^kRescaleLog2, rescale O and l, and
-  // shift the tile's x values to the new offset
+  // rescale test, given the row max mx of a tile's x values (raw scores with
+  // exact scale): move the offset when c (row max) outgrows it -- by any
+  // amount with exact scale, by 2^kRescaleLog2 when folded -- rescale O and
+  // l, and shift the tile's x values to the new offset
   auto rescale_test = [&](float mx, f32x16* X) __attribute__((always_inline)) {
     mx = pair_max(mx);
     const float cand = kExact ? mx * a.c : mx + msub;       // c * row max
-    if (__ballot(cand > m_used + kRescaleLog2)) {
+    if (__ballot(cand > m_used + (kExact ? kRescaleLog2Exact : kRescaleLog2))) {
       const float m_new = fmaxf(m_used, cand);
       const float alpha = (m_new == -INFINITY) ? 1.f : exp2f_fast(m_used - m_new);
       m_used = m_new;

@@ -84,7 +84,7 @@ struct sa_ctx {
   float* part = nullptr;           // split-KV partials
   size_t part_cap = 0;             // bytes
   uint32_t* d_sync = nullptr;      // counters of an attention launch that appends (zero between launches)
-  bool exact_scale = false;        // sa_set_exact_scale
+  bool exact_scale = true;         // sa_set_exact_scale (0: scale folded into q)
   hipEvent_t kernel_ev[2][2] = {};   // sa_set_kernel_events: [SA_TIMED_ATTN | SA_TIMED_PAGES][start, stop]
   uint64_t* blk_clock = nullptr;     // sa_set_block_clock: device buffer, 4 words per block
   float xcd_weight[8] = {1, 1, 1, 1, 1, 1, 1, 1};   // sa_set_xcd_weights: relative XCD speeds

@@ -20,8 +20,17 @@ from harness import (attention, build_cache, build_source_cache, compare, dev_i3
                      sample_rows, score_shift_bound)
 
 
-def check_lse(w, got, ref, toks=None, heads=None):
-    """Device LSE within the bound its bf16-rounded scaled query allows."""
+LSE_TOL = 1e-3      # natural-log units, every row of the default (exact-scale) path
+
+
+def check_lse(w, got, ref, toks=None, heads=None, folded=False):
+    """Device LSE against the oracle's: within LSE_TOL on the default path, where the
+    scale is applied to each fp32 score; with the scale folded into the bf16 query
+    (sa_set_exact_scale(ctx, 0)), within the per-row shift that rounding allows."""
+    if not folded:
+        err = np.abs(np.asarray(got, dtype=np.float64) - ref)
+        assert np.isfinite(got).all() and float(err.max()) <= LSE_TOL, float(err.max())
+        return
     if toks is None:
         T = int(w.q_indptr[-1])
         toks = np.repeat(np.arange(T, dtype=np.int64), w.num_q_heads)
@@ -157,7 +166,7 @@ def test_split_kv_and_merge(ctx):
     check_lse(w, lse.cpu().numpy(), ref_lse)
 
 
-def check_attention_append(ctx, w, launches=2):
+def check_attention_append(ctx, w, launches=2, folded=False):
     """sa_segment_prefill_attn_append over a cache holding only the prefix (layer 1 of
     two): both pools end exactly as the oracle's append leaves them, and every output
     row and LSE matches the oracle.  Each launch starts from fresh pools, so the second
@@ -183,7 +192,7 @@ def check_attention_append(ctx, w, launches=2):
             opages.apply_append(wa[layer], new, sl, ro)
             assert np.array_equal(host_u16(got), wa), n
         mx, mean = compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
-        check_lse(w, lse.cpu().numpy(), ref_lse)
+        check_lse(w, lse.cpu().numpy(), ref_lse, folded=folded)
     print(f"  {w.name}: max {mx:.3e} mean {mean:.3e}", flush=True)
 
 
@@ -199,7 +208,7 @@ def test_append_inside_attention_split_kv(ctx):
     check_attention_append(ctx, build("split", 21, 8, 1, 128, 16, [5000, 3000, 70, 0], [1, 1, 3, 1]))
 
 
-def test_append_inside_attention_missing_page_is_reported(ctx):
+def test_append_inside_attention_missing_page_is_reported(ctx, folded=False):
     """A new row whose page is not in the table is skipped and reported."""
     print("attention with append, missing page", flush=True)
     w = build("short", 51, 8, 2, 128, 16, [20], [40])
@@ -215,7 +224,7 @@ def test_append_inside_attention_missing_page_is_reported(ctx):
         sa.sa_sync_check(ctx)
     assert e.value.name == "SA_ERR_RANGE"
     sa.sa_sync_check(ctx)
-    check_attention_append(ctx, workloads.make("c1"), launches=1)   # the next launch is whole
+    check_attention_append(ctx, workloads.make("c1"), launches=1, folded=folded)   # the next launch is whole
 
 
 def test_first_row_without_prefix_is_v0_bitwise(ctx):
@@ -262,14 +271,13 @@ def test_constant_values_and_zero_keys_closed_forms(ctx):
             compare(bits[int(w.q_indptr[b]) + i], want, MAX_TOL, MEAN_TOL)
 
 
-@pytest.mark.parametrize("scale,std", [(1.0, 1.0), (2.0, 1.0), (1e-4, 1.0)])
+@pytest.mark.parametrize("scale,std", [(1.0, 1.0), (2.0, 1.0), (1e-4, 1.0), (128 ** -0.5, 2.0)])
 def test_large_and_tiny_softmax_scales(ctx, scale, std):
     """Scores spread over tens of powers of two (the running max keeps moving past the
-    lazy-rescale threshold) and nearly uniform weights.  The kernel rounds c q to bf16,
-    so each row's exponents may move by eps = 2^-8 max_j sum_d |c q_d k_jd|: its LSE must
-    stay within ln 2 eps of the oracle's and each output within (2^(2 eps) - 1) max|v| plus
-    the bf16 roundings of P and O (2^-7 max|v|) -- a missed rescale or an overflow would
-    be off by factors of 2^8 or not finite."""
+    lazy-rescale threshold), nearly uniform weights, and inputs four times wider than the
+    configurations' at their scale: every output within max 2e-2 / mean 2e-3 of the
+    oracle and every LSE within 1e-3 (a missed rescale or an overflow would be off by
+    factors of 2^8 or not finite)."""
     w = build(f"scale{scale}", 64, 8, 2, 128, 16, [700, 0, 33], [150, 90, 1], std=std)
     w.scale = scale
     L = layout_of(w)
@@ -277,9 +285,50 @@ def test_large_and_tiny_softmax_scales(ctx, scale, std):
     o, lse = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
     sa.sa_sync_check(ctx)
     ref, ref_lse, _ = oracle_all(w)
+    mx, mean = compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
+    print(f"  scale {scale} std {std}: max {mx:.3e} mean {mean:.3e}", flush=True)
+    check_lse(w, lse.cpu().numpy(), ref_lse)
+
+
+@pytest.fixture(scope="module")
+def ctx_folded():
+    """A context in the fast mode that folds the scale into the bf16 query rows."""
+    c = sa.Context(0)
+    sa.sa_set_exact_scale(c, False)
+    yield c
+    c.close()
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_folded_scale_all_rows(ctx_folded, name):
+    """Folded-scale mode: outputs within the same bars, the LSE within the per-row shift
+    the bf16 rounding of the scaled query allows."""
+    w = small(name)
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    o, lse = attention(ctx_folded, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    sa.sa_sync_check(ctx_folded)
+    ref, ref_lse, _ = oracle_all(w)
+    compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
+    check_lse(w, lse.cpu().numpy(), ref_lse, folded=True)
+
+
+@pytest.mark.parametrize("scale", [1.0, 2.0, 1e-4])
+def test_folded_scale_at_large_and_tiny_scales(ctx_folded, scale):
+    """Folded-scale mode at large logits: each row's exponents may move by
+    eps = 2^-8 max_j sum_d |c q_d k_jd|, so its LSE must stay within ln 2 eps of the
+    oracle's and each output within (2^(2 eps) - 1) max|v| plus the bf16 roundings of P
+    and O (2^-7 max|v|).  This is the mode's documented accuracy, not the default's."""
+    w = build(f"fscale{scale}", 64, 8, 2, 128, 16, [700, 0, 33], [150, 90, 1], std=1.0)
+    w.scale = scale
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    o, lse = attention(ctx_folded, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    sa.sa_sync_check(ctx_folded)
+    ref, ref_lse, _ = oracle_all(w)
     got = (host_u16(o).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
     assert np.isfinite(got).all() and np.isfinite(lse.cpu().numpy()).all()
-    check_lse(w, lse.cpu().numpy(), ref_lse)
+    check_lse(w, lse.cpu().numpy(), ref_lse, folded=True)
     T = int(w.q_indptr[-1])
     toks = np.repeat(np.arange(T, dtype=np.int64), w.num_q_heads)
     heads = np.tile(np.arange(w.num_q_heads, dtype=np.int32), T)
@@ -292,49 +341,10 @@ def test_large_and_tiny_softmax_scales(ctx, scale, std):
         compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
 
 
-@pytest.fixture(scope="module")
-def ctx_exact():
-    c = sa.Context(0)
-    sa.sa_set_exact_scale(c, True)
-    yield c
-    c.close()
-
-
-@pytest.mark.parametrize("name", SMALL)
-def test_exact_scale_all_rows(ctx_exact, name):
-    """The pipelined kernel with the scale applied per score in fp32: same bars, and the
-    LSE within 1e-4 of the oracle (no rounding of the scaled query to allow for)."""
-    w = small(name)
-    L = layout_of(w)
-    kp, vp, ip, ix = build_cache(w)
-    o, lse = attention(ctx_exact, w, L, dev_u16(w.q), kp, vp, ip, ix)
-    sa.sa_sync_check(ctx_exact)
-    ref, ref_lse, _ = oracle_all(w)
-    compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
-    assert np.abs(lse.cpu().numpy() - ref_lse).max() <= 1e-4
-
-
-@pytest.mark.parametrize("scale", [1.0, 2.0, 1e-4])
-def test_exact_scale_at_large_and_tiny_scales(ctx_exact, scale):
-    """Exact scaling keeps the LSE within 1e-4 of the oracle where the folded scale moves
-    it by up to ~0.16; the outputs are then off by the bf16 roundings of P and O only."""
-    w = build(f"xscale{scale}", 64, 8, 2, 128, 16, [700, 0, 33], [150, 90, 1], std=1.0)
-    w.scale = scale
-    L = layout_of(w)
-    kp, vp, ip, ix = build_cache(w)
-    o, lse = attention(ctx_exact, w, L, dev_u16(w.q), kp, vp, ip, ix)
-    sa.sa_sync_check(ctx_exact)
-    ref, ref_lse, _ = oracle_all(w)
-    assert np.abs(lse.cpu().numpy() - ref_lse).max() <= 1e-4
-    got = (host_u16(o).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
-    vmax = np.abs((w.v.astype(np.uint32) << 16).view(np.float32)).max()
-    assert np.abs(got - ref).max() <= 2.0 ** -6 * vmax
-
-
 @pytest.mark.timeout(600)
-def test_exact_scale_step_c2_full(ctx_exact):
-    print("c2 full step, exact scale", flush=True)
-    check_step(ctx_exact, workloads.make("c2"), per_seq_rows=128)
+def test_folded_scale_step_c2_full(ctx_folded):
+    print("c2 full step, folded scale", flush=True)
+    check_step(ctx_folded, workloads.make("c2"), per_seq_rows=128, folded=True)
 
 
 def test_attention_kernel_events(ctx):
@@ -489,7 +499,7 @@ def run_step(ctx, w, L, state, mode="copy"):
     return dst_len
 
 
-def check_step(ctx, w, per_seq_rows, mode="copy"):
+def check_step(ctx, w, per_seq_rows, mode="copy", folded=False):
     alias = mode == "alias"
     L = layout_of(w)
     kp, vp, sip, sid, fresh = build_source_cache(w)
@@ -537,7 +547,7 @@ def check_step(ctx, w, per_seq_rows, mode="copy"):
     got = host_u16(o)[toks, heads]
     mx, mean = compare(got, ref, MAX_TOL, MEAN_TOL)
     print(f"  {w.name}: {len(toks)} rows, max {mx:.3e} mean {mean:.3e}", flush=True)
-    check_lse(w, lse.cpu().numpy()[toks, heads], ref_lse, toks, heads)
+    check_lse(w, lse.cpu().numpy()[toks, heads], ref_lse, toks, heads, folded=folded)
     assert torch.isfinite(o.view(torch.bfloat16).float()).all()
 
 
@@ -766,7 +776,7 @@ def test_step_c3_full(ctx):
     check_step(ctx, workloads.make("c3"), per_seq_rows=48)
 
 
-def check_direct(ctx, w, per_seq_rows, extra_rows=None, fused=False):
+def check_direct(ctx, w, per_seq_rows, extra_rows=None, fused=False, folded=False):
     L = layout_of(w)
     kp, vp, ip, ix = build_cache(w, with_segment=False)
     if fused:
@@ -788,7 +798,7 @@ def check_direct(ctx, w, per_seq_rows, extra_rows=None, fused=False):
                                             w.num_q_heads, w.num_kv_heads, w.scale, toks, heads)
     mx, mean = compare(host_u16(o)[toks, heads], ref, MAX_TOL, MEAN_TOL)
     print(f"  {w.name}: {len(toks)} rows, max {mx:.3e} mean {mean:.3e}", flush=True)
-    check_lse(w, lse.cpu().numpy()[toks, heads], ref_lse, toks, heads)
+    check_lse(w, lse.cpu().numpy()[toks, heads], ref_lse, toks, heads, folded=folded)
     assert torch.isfinite(o.view(torch.bfloat16).float()).all()
 
 

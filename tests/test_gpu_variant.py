@@ -44,11 +44,11 @@ for name, w in cases:
     ref, ref_lse, _ = oracle.attention_all(w.q, w.k, w.v, w.q_indptr, w.kv_indptr,
                                            w.num_q_heads, w.num_kv_heads, w.scale)
     mx, mean = compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
-    check_lse(w, lse.cpu().numpy(), ref_lse)
+    check_lse(w, lse.cpu().numpy(), ref_lse, folded={folded})
     print("  ok max %.3e mean %.3e" % (mx, mean), flush=True)
 from test_gpu_parity import check_attention_append
 print("variant {variant} attention with append (separate append launch)", flush=True)
-check_attention_append(ctx, small("ragged_g4_p16"))
+check_attention_append(ctx, small("ragged_g4_p16"), folded={folded})
 ctx.close()
 print("ALL-OK", flush=True)
 """
@@ -57,7 +57,8 @@ print("ALL-OK", flush=True)
 @pytest.mark.timeout(300)
 @pytest.mark.parametrize("variant", [1, 2])
 def test_variant_kernel_parity(variant):
-    code = CHILD.format(root=ROOT, tests=os.path.join(ROOT, "tests"), variant=variant)
+    # variant 1 always scales each score in fp32, variant 2 always folds the scale into q
+    code = CHILD.format(root=ROOT, tests=os.path.join(ROOT, "tests"), variant=variant, folded=variant == 2)
     env = dict(os.environ, SA_ATTN_VARIANT=str(variant))
     r = subprocess.run([sys.executable, "-u", "-c", code], env=env, cwd=ROOT,
                        capture_output=True, text=True, timeout=280)
@@ -75,29 +76,30 @@ from workloads.configs import build
 from test_gpu_parity import (small, SMALL, check_attention_append, check_step, check_direct,
                              test_append_inside_attention_missing_page_is_reported)
 ctx = sa.Context(0)
+sa.sa_set_exact_scale(ctx, False)      # the single-launch append runs in the folded-scale mode
 for n in SMALL:
     print("append in attention", n, flush=True)
-    check_attention_append(ctx, small(n))
+    check_attention_append(ctx, small(n), folded=True)
 print("append in attention, split", flush=True)
-check_attention_append(ctx, build("split", 21, 8, 1, 128, 16, [5000, 3000, 70, 0], [1, 1, 3, 1]))
+check_attention_append(ctx, build("split", 21, 8, 1, 128, 16, [5000, 3000, 70, 0], [1, 1, 3, 1]), folded=True)
 print("append in attention, missing page", flush=True)
-test_append_inside_attention_missing_page_is_reported(ctx)
+test_append_inside_attention_missing_page_is_reported(ctx, folded=True)
 from test_gpu_parity import random_case
 import numpy as np
 for k in range(6):
     print("append in attention, random shape", k, flush=True)
-    check_attention_append(ctx, random_case(k), launches=1)
+    check_attention_append(ctx, random_case(k), launches=1, folded=True)
 for k in range(4):
     r = np.random.default_rng(9100 + k)
     B = int(r.integers(2, 7))
     pre = [int(x) for x in r.integers(0, 4001, B)]
     ql = [1 if r.random() < 0.5 else int(r.integers(2, 201)) for _ in range(B)]
     print("append in attention, mixed decode/prefill", k, pre, ql, flush=True)
-    check_attention_append(ctx, build("amix%d" % k, 9100 + k, 16, 4, 128, 16, pre, ql), launches=1)
+    check_attention_append(ctx, build("amix%d" % k, 9100 + k, 16, 4, 128, 16, pre, ql), launches=1, folded=True)
 print("append in attention, c2 step", flush=True)
-check_step(ctx, workloads.make("c2"), per_seq_rows=128, mode="attn_append")
+check_step(ctx, workloads.make("c2"), per_seq_rows=128, mode="attn_append", folded=True)
 print("append in attention, c5", flush=True)
-check_direct(ctx, workloads.make("c5"), per_seq_rows=16, fused=True)
+check_direct(ctx, workloads.make("c5"), per_seq_rows=16, fused=True, folded=True)
 ctx.close()
 print("ALL-OK", flush=True)
 """
