@@ -53,7 +53,17 @@
  *   - Page ids inside device tables are range-checked by the kernels: a page
  *     beyond a sequence's list or a slot outside [0, num_slots) is skipped
  *     (never dereferenced) and latched in a device flag that sa_sync_check
- *     reports.  Reads of such pages contribute zeros.
+ *     reports.  Reads of such pages contribute zeros.  Nothing on the hot
+ *     path checks that slots do not repeat; with the environment variable
+ *     SA_DEBUG=1 (read once per process) every splice and append first copies
+ *     the tables it will use back to the host (synchronising its stream) and
+ *     refuses, before launching, slots outside the pool or pages a sequence
+ *     lacks (SA_ERR_RANGE), a free list that repeats a slot or hands out a
+ *     surviving source slot, and two sequences writing the same row of a slot
+ *     (SA_ERR_OVERLAP).
+ *   - Plan buffers grow on demand (hipMalloc) and an outgrown one is kept
+ *     until sa_destroy, since kernels already enqueued may still read it; no
+ *     call synchronises the device.  sa_reserve sizes them ahead of time.
  *   - Pointers to pools, Q, O, K/V rows must be 16-byte aligned.
  */
 #ifndef SA_H
@@ -74,7 +84,8 @@ typedef enum sa_status {
     SA_ERR_RANGE = 5,         /* a span or page id is out of range                      */
     SA_ERR_NO_PAGES = 6,      /* free list or destination table too small               */
     SA_ERR_HIP = 7,           /* a HIP runtime call failed (see sa_last_error)          */
-    SA_ERR_DEVICE = 8         /* no usable gfx950 device                                 */
+    SA_ERR_DEVICE = 8,        /* no usable gfx950 device                                 */
+    SA_ERR_OVERLAP = 9        /* slot lists repeat where they must not (SA_DEBUG checks) */
 } sa_status;
 
 typedef struct sa_ctx sa_ctx;
@@ -108,6 +119,21 @@ const char *sa_status_string(sa_status status);
 
 /* Message of the most recent failing call on this thread ("" if none). */
 const char *sa_last_error(void);
+
+/*
+ * sa_reserve — size the context's buffers ahead of time, so that later calls
+ * whose plans fit them allocate no device or pinned memory (for example
+ * before a timed loop or a serving loop).  plan_bytes: capacity of each call
+ * kind's device plan buffer and of each pinned staging buffer; an attention
+ * call's plan takes about 40 bytes per work item (one per sequence, KV head
+ * and 128 packed query rows, and per key-range part of a split item) plus
+ * 16 bytes per sequence, 24 per split item and 768 of alignment; a splice's
+ * about 24 bytes per surviving page plus 16 per sequence.  split_bytes:
+ * capacity of the split-KV partials, 128 * 129 * 4 bytes per key-range part.
+ * Buffers only grow; outgrown ones are kept until sa_destroy.
+ * Errors: SA_ERR_NULL (context), SA_ERR_SHAPE (negative size), SA_ERR_HIP.
+ */
+sa_status sa_reserve(sa_ctx *ctx, int64_t plan_bytes, int64_t split_bytes);
 
 /* Wait for `stream`, then report SA_ERR_RANGE if any kernel of this context
  * met an out-of-range page id or slot since the last check (and clear it). */
@@ -155,7 +181,8 @@ sa_status sa_kv_append(sa_ctx *ctx, const sa_layout *layout, int32_t layer,
  *
  * k_dst / v_dst may be the same pools as k_src / v_src.  Fresh slots must not
  * be surviving source slots of this call (the copy reads and writes in
- * parallel); nothing checks this on the hot path.
+ * parallel) and must not repeat; nothing checks this on the hot path
+ * (SA_DEBUG=1 does, see the conventions above).
  *
  * Errors: SA_ERR_SHAPE, SA_ERR_RANGE (bad span), SA_ERR_NO_PAGES (free list
  * or dst_capacity too small), SA_ERR_UNSUPPORTED, SA_ERR_NULL, SA_ERR_ALIGN,

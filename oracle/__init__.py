@@ -21,25 +21,32 @@ from . import pages  # noqa: F401  (re-exported)
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
+# AddressSanitizer + UndefinedBehaviorSanitizer build, loaded instead of the
+# plain one when ORACLE_SANITIZED=1 (the process must then preload libasan)
+_LIB_SAN = os.path.join(_HERE, "liboracle_san.so")
 _lib = None
 
 
-def build(force: bool = True) -> str:
+def build(force: bool = True, sanitize: bool = False) -> str:
     """Compile oracle.c with gcc (no fast-math: IEEE double, source order)."""
-    if force or not os.path.exists(_LIB):
-        tmp = _LIB + f".tmp{os.getpid()}"
-        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11",
+    out = _LIB_SAN if sanitize else _LIB
+    if force or not os.path.exists(out):
+        tmp = out + f".tmp{os.getpid()}"
+        flags = ["-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+                 "-fno-omit-frame-pointer"] if sanitize else ["-O2"]
+        subprocess.check_call(["gcc", *flags, "-fopenmp", "-fPIC", "-shared", "-std=c11",
                                "-Wall", "-Werror", _SRC, "-o", tmp, "-lm"])
-        os.replace(tmp, _LIB)
-    return _LIB
+        os.replace(tmp, out)
+    return out
 
 
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB):
-            build(force=True)
-        lib = ctypes.CDLL(_LIB)
+        path = _LIB_SAN if os.environ.get("ORACLE_SANITIZED") == "1" else _LIB
+        if not os.path.exists(path):
+            build(force=True, sanitize=path == _LIB_SAN)
+        lib = ctypes.CDLL(path)
         p = ctypes.c_void_p
         lib.oracle_attn_rows.argtypes = [p, p, p, ctypes.c_int, p, p, ctypes.c_int, ctypes.c_int,
                                          ctypes.c_int, ctypes.c_double, ctypes.c_int64, p, p, p, p, p]

@@ -16,7 +16,7 @@ __all__ = [
     "Layout", "Context", "SaError", "library_path", "load_library",
     "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append", "sa_kv_splice_alias",
     "sa_segment_prefill_attn", "sa_segment_prefill_attn_append", "sa_set_exact_scale", "sa_set_kernel_events",
-    "sa_set_block_clock", "sa_set_xcd_weights", "sa_sync_check", "EXPORTED_SYMBOLS",
+    "sa_set_block_clock", "sa_set_xcd_weights", "sa_sync_check", "sa_reserve", "EXPORTED_SYMBOLS",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -27,11 +27,11 @@ EXPORTED_SYMBOLS = ("sa_create", "sa_destroy", "sa_status_string", "sa_last_erro
                     "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
                     "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append",
                     "sa_set_exact_scale", "sa_set_kernel_events", "sa_set_block_clock",
-                    "sa_set_xcd_weights")
+                    "sa_set_xcd_weights", "sa_reserve")
 
 STATUS = {0: "SA_OK", 1: "SA_ERR_NULL", 2: "SA_ERR_SHAPE", 3: "SA_ERR_UNSUPPORTED",
           4: "SA_ERR_ALIGN", 5: "SA_ERR_RANGE", 6: "SA_ERR_NO_PAGES", 7: "SA_ERR_HIP",
-          8: "SA_ERR_DEVICE"}
+          8: "SA_ERR_DEVICE", 9: "SA_ERR_OVERLAP"}
 
 
 class SaError(RuntimeError):
@@ -87,9 +87,11 @@ def load_library():
     lib.sa_set_kernel_events.argtypes = [P, I32, P, P]
     lib.sa_set_block_clock.argtypes = [P, P, I64, ctypes.POINTER(ctypes.c_int64)]
     lib.sa_set_xcd_weights.argtypes = [P, P]
+    lib.sa_reserve.argtypes = [P, I64, I64]
     for name in ("sa_create", "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
                  "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append",
-                 "sa_set_exact_scale", "sa_set_kernel_events", "sa_set_block_clock", "sa_set_xcd_weights"):
+                 "sa_set_exact_scale", "sa_set_kernel_events", "sa_set_block_clock", "sa_set_xcd_weights",
+                 "sa_reserve"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -198,6 +200,12 @@ def _ctx_handle(ctx):
     if ctx is None:
         return None
     return ctx.handle if isinstance(ctx, Context) else ctx
+
+
+def sa_reserve(ctx, plan_bytes: int, split_bytes: int = 0):
+    """Size ctx's plan buffers (each call kind's, and the pinned staging) to plan_bytes and
+    its split-KV partials to split_bytes, so later calls that fit allocate nothing."""
+    _check(load_library().sa_reserve(_ctx_handle(ctx), int(plan_bytes), int(split_bytes)))
 
 
 def sa_sync_check(ctx, stream=None):

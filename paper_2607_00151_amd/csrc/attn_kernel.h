@@ -35,32 +35,9 @@
 #include <stdint.h>
 
 #include "common.h"
+#include "plan.h"
 
 namespace sa {
-
-constexpr int kHD = 128;          // head dim
-constexpr int kKT = 64;           // keys per tile
-constexpr int kMaxRows = 256;     // largest query-row tile of a work item
-
-struct AttnItem {
-  int32_t seq;
-  int32_t kvh;
-  int32_t row0;      // first packed row
-  int32_t kv_begin;  // first key, multiple of kKT
-  int32_t kv_end;    // one past the last key this item reads (<= kv_len)
-  int32_t part;      // -1: final output; else index of this item's partial slot
-  int32_t boost;     // steps at the start that run at raised wave priority (0: none)
-  int32_t q_start;   // the sequence's SeqDesc fields, repeated so that one read
-  int32_t q_len;     // of the item gives a workgroup all it needs to start
-  int32_t kv_len;
-};
-
-struct SeqDesc {
-  int32_t q_start;   // first token of the sequence in Q / O
-  int32_t q_len;
-  int32_t kv_len;
-  int32_t pad;
-};
 
 struct AttnArgs {
   const uint16_t* q;
@@ -415,10 +392,6 @@ __global__ __launch_bounds__(64 * WAVES, (QT == 1 ? 2 : 1)) void attn_kernel(Att
 }
 
 // Combine the key-range partials of split work items by their log-sum-exp.
-struct MergeGroup {
-  int32_t seq, kvh, row0, nsplit, part0, pad;
-};
-
 struct MergeArgs {
   const float* part_o;
   const float* part_lse;

@@ -8,6 +8,7 @@
 #include <stdint.h>
 
 #include "common.h"
+#include "plan.h"
 
 namespace sa {
 
@@ -83,16 +84,6 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
 
 // One copied page: which sequence, its logical source page, and its position
 // in the destination table (also its index into the fresh-slot list).
-struct AsmUnit {
-  int32_t seq;
-  int32_t src_page;
-  int32_t dst_index;
-  // with an append in the same launch: rows app_row0 .. app_row0 + app_rows - 1
-  // of this page (the last surviving one, when partial) come from new-row
-  // token app_tok onwards instead of from the source page
-  int32_t app_row0, app_rows, app_tok;
-};
-
 struct AsmArgs {
   const uint16_t* k_src;
   const uint16_t* v_src;

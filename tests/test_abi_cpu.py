@@ -36,7 +36,7 @@ def test_header_and_library_agree(lib):
 
 
 def test_status_strings(lib):
-    for code in range(9):
+    for code in range(10):
         assert lib.sa_status_string(code)
     assert lib.sa_status_string(99) == b"unknown status"
 
