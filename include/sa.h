@@ -279,6 +279,33 @@ sa_status sa_segment_prefill_attn(sa_ctx *ctx, const sa_layout *layout, int32_t 
                                   void *o, float *lse, void *stream);
 
 /*
+ * sa_segment_prefill_attn_noalloc — sa_segment_prefill_attn for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Same arguments, same results (bit
+ * for bit as long as its split-KV partials fit, see below), but it calls no
+ * hipMalloc, hipFree or other allocating HIP routine (the host planner uses
+ * only ordinary C++ heap memory): the launch's plan and its split-KV partials
+ * live in one fixed device array of 32 MiB per GPU, a file-scope
+ * `static __device__` array that each GPU the library runs on holds until
+ * the process ends; the plan reaches it through pinned staging the context
+ * allocated at sa_create.  Limits: the plan (about 40 bytes per work item, a
+ * work item per sequence, KV head and 128 packed query rows) must fit 2 MiB,
+ * else SA_ERR_SHAPE before anything is enqueued; the partials get the other
+ * 30 MiB (476 key-range parts of 128 rows), and a launch that would split
+ * into more parts is split more coarsely instead.  Every call on one GPU uses
+ * that GPU's array, whichever context makes it, and leaves the last call's
+ * contents there: calls that overlap in time on one GPU (two streams, two
+ * contexts) race, so order them.  The call may wait on the host for the
+ * previous plan copy of the same context to finish.
+ * Errors: those of sa_segment_prefill_attn.
+ */
+sa_status sa_segment_prefill_attn_noalloc(sa_ctx *ctx, const sa_layout *layout, int32_t layer,
+                                          const void *q, const void *k_pool, const void *v_pool,
+                                          int32_t batch, const int32_t *h_q_len, const int32_t *h_kv_len,
+                                          sa_pages pages, float softmax_scale,
+                                          void *o, float *lse, void *stream);
+
+/*
  * sa_set_exact_scale — how later attention calls on this context apply
  * softmax_scale.  enable != 0 (the default) multiplies each fp32 score by it
  * (with log2(e)) before the exponential: the only roundings are those of the

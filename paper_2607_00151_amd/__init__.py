@@ -16,7 +16,8 @@ __all__ = [
     "Layout", "Context", "SaError", "library_path", "load_library",
     "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append", "sa_kv_splice_alias",
     "sa_segment_prefill_attn", "sa_segment_prefill_attn_append", "sa_set_exact_scale", "sa_set_kernel_events",
-    "sa_set_block_clock", "sa_set_xcd_weights", "sa_sync_check", "sa_reserve", "EXPORTED_SYMBOLS",
+    "sa_set_block_clock", "sa_set_xcd_weights", "sa_sync_check", "sa_reserve",
+    "sa_segment_prefill_attn_noalloc", "EXPORTED_SYMBOLS",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -27,7 +28,7 @@ EXPORTED_SYMBOLS = ("sa_create", "sa_destroy", "sa_status_string", "sa_last_erro
                     "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
                     "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append",
                     "sa_set_exact_scale", "sa_set_kernel_events", "sa_set_block_clock",
-                    "sa_set_xcd_weights", "sa_reserve")
+                    "sa_set_xcd_weights", "sa_reserve", "sa_segment_prefill_attn_noalloc")
 
 STATUS = {0: "SA_OK", 1: "SA_ERR_NULL", 2: "SA_ERR_SHAPE", 3: "SA_ERR_UNSUPPORTED",
           4: "SA_ERR_ALIGN", 5: "SA_ERR_RANGE", 6: "SA_ERR_NO_PAGES", 7: "SA_ERR_HIP",
@@ -88,10 +89,11 @@ def load_library():
     lib.sa_set_block_clock.argtypes = [P, P, I64, ctypes.POINTER(ctypes.c_int64)]
     lib.sa_set_xcd_weights.argtypes = [P, P]
     lib.sa_reserve.argtypes = [P, I64, I64]
+    lib.sa_segment_prefill_attn_noalloc.argtypes = lib.sa_segment_prefill_attn.argtypes
     for name in ("sa_create", "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
                  "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append",
                  "sa_set_exact_scale", "sa_set_kernel_events", "sa_set_block_clock", "sa_set_xcd_weights",
-                 "sa_reserve"):
+                 "sa_reserve", "sa_segment_prefill_attn_noalloc"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -324,6 +326,21 @@ def sa_segment_prefill_attn(ctx, layout: Layout, layer: int, q, k_pool, v_pool, 
     qp, op, lp, _ = _attn_dev(layout, q_len, q, o, lse)
     n = _pool_numel(layout)
     _check(load_library().sa_segment_prefill_attn(
+        _ctx_handle(ctx), ctypes.byref(layout), int(layer), qp, _dev(k_pool, "k_pool", "b16", n),
+        _dev(v_pool, "v_pool", "b16", n), int(len(q_len)), _ptr(q_len), _ptr(kv_len),
+        _pages(pages_indptr, pages_indices, len(q_len)), float(softmax_scale), op, lp, _stream(stream)))
+
+
+def sa_segment_prefill_attn_noalloc(ctx, layout: Layout, layer: int, q, k_pool, v_pool, q_len, kv_len,
+                                    pages_indptr, pages_indices, softmax_scale: float, o, lse=None, stream=None):
+    """sa_segment_prefill_attn without any device allocation: plan and split partials in the
+    library's fixed per-GPU scratch array (calls on one GPU must not overlap in time)."""
+    q_len, kv_len = _host_i32(q_len), _host_i32(kv_len)
+    if q_len.shape != kv_len.shape:
+        raise ValueError("q_len and kv_len differ in length")
+    qp, op, lp, _ = _attn_dev(layout, q_len, q, o, lse)
+    n = _pool_numel(layout)
+    _check(load_library().sa_segment_prefill_attn_noalloc(
         _ctx_handle(ctx), ctypes.byref(layout), int(layer), qp, _dev(k_pool, "k_pool", "b16", n),
         _dev(v_pool, "v_pool", "b16", n), int(len(q_len)), _ptr(q_len), _ptr(kv_len),
         _pages(pages_indptr, pages_indices, len(q_len)), float(softmax_scale), op, lp, _stream(stream)))

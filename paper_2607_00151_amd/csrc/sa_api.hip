@@ -12,6 +12,7 @@
 #include <cstring>
 #include <string>
 #include <map>
+#include <mutex>
 #include <vector>
 
 #include "sa.h"
@@ -61,6 +62,41 @@ struct PlanImage {
 
 enum PlanKind { kPlanAppend = 0, kPlanAssemble = 1, kPlanAttn = 2, kPlanAlias = 3, kPlanKinds = 4 };
 
+// Fixed device scratch of sa_segment_prefill_attn_noalloc: the launch's plan
+// (sequence records, work items, merge groups) in its first kNoAllocPlanBytes,
+// the key-range partials of split items after it.  Every device the library
+// runs on holds one copy for the life of the process, shared by all contexts
+// on that device.
+constexpr size_t kNoAllocBytes = size_t(32) << 20;
+constexpr size_t kNoAllocPlanBytes = size_t(2) << 20;
+constexpr int kMaxDevices = 64;
+
+}  // namespace
+
+static __device__ __align__(256) uint8_t scratch[kNoAllocBytes];
+
+namespace {
+
+// Device address of `scratch` on each device: the array's name is only a
+// host-side stand-in, so host code uses this address (looked up once per
+// device, with that device current) wherever it needs the array's memory.
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+hipError_t scratch_address(int device, void** out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  if (g_scratch_ptr[device] == nullptr) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (ptr == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[device] = ptr;
+  }
+  *out = g_scratch_ptr[device];
+  return hipSuccess;
+}
+
 }  // namespace
 
 struct sa_ctx {
@@ -92,6 +128,12 @@ struct sa_ctx {
   // buffers outgrown by a larger plan: kernels already enqueued may still read
   // them, so they are freed with the context rather than behind a device sync
   std::vector<void*> retired_dev, retired_host;
+  // sa_segment_prefill_attn_noalloc: this device's `scratch` array, and pinned
+  // staging for the plans copied into it
+  uint8_t* scratch = nullptr;
+  void* na_host = nullptr;
+  hipEvent_t na_ev = nullptr;
+  bool na_pending = false;
 };
 
 namespace {
@@ -318,6 +360,9 @@ sa_status sa_create(int device, sa_ctx** out) {
   if (e == hipSuccess) e = hipDeviceSynchronize();
   for (int i = 0; e == hipSuccess && i < kRing; ++i)
     e = hipEventCreateWithFlags(&c->ring[i].ev, hipEventDisableTiming);
+  if (e == hipSuccess) e = scratch_address(device, (void**)&c->scratch);
+  if (e == hipSuccess) e = hipHostMalloc(&c->na_host, kNoAllocPlanBytes, hipHostMallocDefault);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->na_ev, hipEventDisableTiming);
   if (e != hipSuccess) {
     sa_destroy(c);
     return fail(SA_ERR_HIP, "context setup failed: %s", hipGetErrorString(e));
@@ -341,6 +386,8 @@ void sa_destroy(sa_ctx* ctx) {
   for (void* p : ctx->retired_host) (void)hipHostFree(p);
   if (ctx->d_sync) (void)hipFree(ctx->d_sync);
   if (ctx->d_err) (void)hipFree(ctx->d_err);
+  if (ctx->na_host) (void)hipHostFree(ctx->na_host);
+  if (ctx->na_ev) (void)hipEventDestroy(ctx->na_ev);
   delete ctx;
 }
 
@@ -648,10 +695,15 @@ namespace {
 // new K/V rows (k_new, v_new) to its positions kv_len - q_len .. kv_len - 1:
 // as an append launch before the attention, or inside the attention launch
 // (append_in_attention()).
+//
+// With `noalloc` the plan and the split partials go to this device's fixed
+// `scratch` array (no append then): the plan must fit kNoAllocPlanBytes, and
+// split items are coarsened until their partials fit the rest.
 sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const void* q,
                       const void* k_pool, const void* v_pool, bool append, const void* k_new,
                       const void* v_new, int32_t batch, const int32_t* h_q_len, const int32_t* h_kv_len,
-                      sa_pages pages, float softmax_scale, void* o, float* lse, void* stream) {
+                      sa_pages pages, float softmax_scale, void* o, float* lse, void* stream,
+                      bool noalloc = false) {
   std::vector<sa::SeqDesc> seqs;
   int64_t total_q = 0;
   sa_status s = sa::plan_attn_check(layout, layer, batch, h_q_len, h_kv_len, softmax_scale, seqs, total_q, g_err);
@@ -689,13 +741,15 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
   shape.rows_item = rows_item;
   shape.num_cu = ctx->num_cu;
   shape.pair_rounds = var.pipe != 2;      // the two-group kernel runs one block per CU
+  const size_t part_bytes = (size_t)rows_item * (sa::kHD + 1) * sizeof(float);   // one key-range part
+  if (noalloc) shape.max_parts = (int64_t)((kNoAllocBytes - kNoAllocPlanBytes) / part_bytes);
   sa::AttnPlan plan;
   sa::plan_attn_items(layout, seqs, shape, &ctx->xcd, plan);
   std::vector<sa::AttnItem>& items = plan.items;
   std::vector<sa::MergeGroup>& groups = plan.groups;
   const int32_t n_parts = plan.n_parts;
 
-  if (n_parts > 0) {
+  if (n_parts > 0 && !noalloc) {
     const size_t need = (size_t)n_parts * rows_item * (sa::kHD + 1) * sizeof(float);
     if (need > ctx->part_cap) {
       if (ctx->part) ctx->retired_dev.push_back(ctx->part);    // an enqueued merge may still read it
@@ -711,8 +765,29 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
   const size_t o_it = img.add(items.data(), items.size());
   const size_t o_gr = img.add(groups.data(), groups.size());
   uint8_t* dev = nullptr;
-  s = upload_plan(ctx, kPlanAttn, img, (hipStream_t)stream, &dev);
-  if (s != SA_OK) return s;
+  float* part = ctx->part;
+  if (noalloc) {
+    // the plan goes to the front of the fixed scratch, through pinned staging
+    // whose previous copy must have been read first; the partials follow it
+    const size_t n = img.bytes.size();
+    if (n > kNoAllocPlanBytes)
+      return fail(SA_ERR_SHAPE, "the launch's plan needs %zu bytes; the fixed scratch of the allocation-free "
+                  "entry point holds %zu (about %zu work items)", n, kNoAllocPlanBytes,
+                  kNoAllocPlanBytes / sizeof(sa::AttnItem));
+    if (ctx->na_pending) {
+      SA_HIP(hipEventSynchronize(ctx->na_ev));
+      ctx->na_pending = false;
+    }
+    memcpy(ctx->na_host, img.bytes.data(), n);
+    SA_HIP(hipMemcpyAsync(ctx->scratch, ctx->na_host, n, hipMemcpyHostToDevice, (hipStream_t)stream));
+    SA_HIP(hipEventRecord(ctx->na_ev, (hipStream_t)stream));
+    ctx->na_pending = true;
+    dev = ctx->scratch;
+    part = (float*)(ctx->scratch + kNoAllocPlanBytes);
+  } else {
+    s = upload_plan(ctx, kPlanAttn, img, (hipStream_t)stream, &dev);
+    if (s != SA_OK) return s;
+  }
 
   sa::AttnArgs a{};
   const int64_t lo = (int64_t)layer * layer_elems(layout);
@@ -721,8 +796,8 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
   a.v = (const uint16_t*)v_pool + lo;
   a.o = (uint16_t*)o;
   a.lse = lse;
-  a.part_o = ctx->part;
-  a.part_lse = ctx->part ? ctx->part + (size_t)n_parts * rows_item * sa::kHD : nullptr;
+  a.part_o = n_parts > 0 ? part : nullptr;
+  a.part_lse = n_parts > 0 ? part + (size_t)n_parts * rows_item * sa::kHD : nullptr;
   a.items = (const sa::AttnItem*)(dev + o_it);
   a.seqs = (const sa::SeqDesc*)(dev + o_seq);
   a.indptr = pages.indptr;
@@ -784,6 +859,15 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
                                   void* stream) {
   return attn_launch(ctx, layout, layer, q, k_pool, v_pool, false, nullptr, nullptr, batch, h_q_len,
                      h_kv_len, pages, softmax_scale, o, lse, stream);
+}
+
+sa_status sa_segment_prefill_attn_noalloc(sa_ctx* ctx, const sa_layout* layout, int32_t layer,
+                                          const void* q, const void* k_pool, const void* v_pool,
+                                          int32_t batch, const int32_t* h_q_len, const int32_t* h_kv_len,
+                                          sa_pages pages, float softmax_scale, void* o, float* lse,
+                                          void* stream) {
+  return attn_launch(ctx, layout, layer, q, k_pool, v_pool, false, nullptr, nullptr, batch, h_q_len, h_kv_len,
+                     pages, softmax_scale, o, lse, stream, true);
 }
 
 sa_status sa_set_exact_scale(sa_ctx* ctx, int32_t enable) {
