@@ -135,6 +135,22 @@ const char *sa_last_error(void);
  */
 sa_status sa_reserve(sa_ctx *ctx, int64_t plan_bytes, int64_t split_bytes);
 
+/*
+ * sa_attn_plan_stats — the shape of the attention launch sa_segment_prefill_attn
+ * would make for these lengths on a GPU with num_cu compute units (host only:
+ * no context, no GPU), for latency models of a batch (paper Sec. 4, Eq. 1
+ * models a batch from its decode and prefill work; how the work falls onto
+ * the chip's workgroup slots adds to that).  out[0]: workgroups; out[1]:
+ * key-range parts of split items (when > 0, a partial-merge launch follows);
+ * out[2]: 64-key tiles over all items; out[3]: makespan in tiles when the
+ * items are taken in launch order by whichever of the 2 x num_cu workgroup
+ * slots frees first (a decode item's tiles count a quarter: its four waves
+ * split them).  Errors: those of sa_segment_prefill_attn's shape checks;
+ * SA_ERR_NULL for a NULL out; SA_ERR_SHAPE for num_cu < 1.
+ */
+sa_status sa_attn_plan_stats(const sa_layout *layout, int32_t batch, const int32_t *h_q_len,
+                             const int32_t *h_kv_len, int32_t num_cu, int64_t *out);
+
 /* Wait for `stream`, then report SA_ERR_RANGE if any kernel of this context
  * met an out-of-range page id or slot since the last check (and clear it). */
 sa_status sa_sync_check(sa_ctx *ctx, void *stream);

@@ -17,7 +17,7 @@ __all__ = [
     "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append", "sa_kv_splice_alias",
     "sa_segment_prefill_attn", "sa_segment_prefill_attn_append", "sa_set_exact_scale", "sa_set_kernel_events",
     "sa_set_block_clock", "sa_set_xcd_weights", "sa_sync_check", "sa_reserve",
-    "sa_segment_prefill_attn_noalloc", "EXPORTED_SYMBOLS",
+    "sa_segment_prefill_attn_noalloc", "sa_attn_plan_stats", "EXPORTED_SYMBOLS",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -28,7 +28,8 @@ EXPORTED_SYMBOLS = ("sa_create", "sa_destroy", "sa_status_string", "sa_last_erro
                     "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
                     "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append",
                     "sa_set_exact_scale", "sa_set_kernel_events", "sa_set_block_clock",
-                    "sa_set_xcd_weights", "sa_reserve", "sa_segment_prefill_attn_noalloc")
+                    "sa_set_xcd_weights", "sa_reserve", "sa_segment_prefill_attn_noalloc",
+                    "sa_attn_plan_stats")
 
 STATUS = {0: "SA_OK", 1: "SA_ERR_NULL", 2: "SA_ERR_SHAPE", 3: "SA_ERR_UNSUPPORTED",
           4: "SA_ERR_ALIGN", 5: "SA_ERR_RANGE", 6: "SA_ERR_NO_PAGES", 7: "SA_ERR_HIP",
@@ -90,10 +91,11 @@ def load_library():
     lib.sa_set_xcd_weights.argtypes = [P, P]
     lib.sa_reserve.argtypes = [P, I64, I64]
     lib.sa_segment_prefill_attn_noalloc.argtypes = lib.sa_segment_prefill_attn.argtypes
+    lib.sa_attn_plan_stats.argtypes = [LP, I32, P, P, I32, P]
     for name in ("sa_create", "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
                  "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append",
                  "sa_set_exact_scale", "sa_set_kernel_events", "sa_set_block_clock", "sa_set_xcd_weights",
-                 "sa_reserve", "sa_segment_prefill_attn_noalloc"):
+                 "sa_reserve", "sa_segment_prefill_attn_noalloc", "sa_attn_plan_stats"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -208,6 +210,18 @@ def sa_reserve(ctx, plan_bytes: int, split_bytes: int = 0):
     """Size ctx's plan buffers (each call kind's, and the pinned staging) to plan_bytes and
     its split-KV partials to split_bytes, so later calls that fit allocate nothing."""
     _check(load_library().sa_reserve(_ctx_handle(ctx), int(plan_bytes), int(split_bytes)))
+
+
+def sa_attn_plan_stats(layout: Layout, q_len, kv_len, num_cu: int = 256) -> dict:
+    """Shape of the attention launch these lengths make (host only, no GPU): workgroups,
+    split parts, 64-key tiles and the makespan in tiles over 2 x num_cu slots."""
+    q_len, kv_len = _host_i32(q_len), _host_i32(kv_len)
+    if q_len.shape != kv_len.shape:
+        raise ValueError("q_len and kv_len differ in length")
+    out = np.zeros(4, dtype=np.int64)
+    _check(load_library().sa_attn_plan_stats(ctypes.byref(layout), int(len(q_len)), _ptr(q_len), _ptr(kv_len),
+                                             int(num_cu), out.ctypes.data))
+    return {"items": int(out[0]), "parts": int(out[1]), "tiles": int(out[2]), "makespan_tiles": int(out[3])}
 
 
 def sa_sync_check(ctx, stream=None):

@@ -826,6 +826,310 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
   }
 }
 
+// ---- work items of at most 32 packed rows (decode requests)
+//
+// A decode request has one query token, so its item holds the G query heads
+// of one KV head -- a single 32-row MFMA block -- over the whole cached
+// context.  Run like a prefill item, one wave would carry every matrix
+// instruction of the item on one SIMD while the other three only load tiles,
+// and a prefill block sharing the CU, whose waves wait on each other at every
+// barrier, would run at the pace of its wave on that SIMD.  Here the four
+// waves split the item's keys instead: wave w takes the 32-key tiles
+// u0 + w, u0 + w + 4, ..., keeps its own online-softmax state over the same
+// rows, and needs no barrier.  Its K tiles go straight into registers (they
+// are the A operand of S^T = K Q^T, so no LDS round trip is needed) and its V
+// tiles into two 8 KB LDS slices of its own (the PV product reads them
+// transposed); K is requested one tile ahead and V two, so a wave keeps up to
+// 24 KB in flight.  The four partial results are merged through LDS at
+// the end.  The item stays bound by HBM, and its matrix work falls evenly on
+// the CU's four SIMDs.
+constexpr int kDecRows = kDecodeRows;        // rows of an item this path takes
+constexpr int kDecKeys = 32;                 // keys per tile of one wave
+
+template <int P, bool kExact>
+__device__ __attribute__((always_inline)) inline void decode_group(const AttnArgs& a, const AttnItem& it,
+                                                                   const SeqDesc& sd, const PipeLds& L) {
+  static_assert(P == 16 || P == 32, "page size");
+  constexpr int kWaves = 4;
+  constexpr int kPagesPerTile = kDecKeys / P;                // 2 or 1
+  constexpr int kSliceBytes = kDecKeys * kHD * 2;            // 8 KB: one V tile of one wave
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & (kWaves - 1);
+  const int hh = lane >> 5;
+  const int G = a.G;
+  const int rows_total = sd.q_len * G;
+  const int pre = sd.kv_len - sd.q_len;
+
+  // every wave holds the same rows: row r of the block is lane r % 32
+  const int r_row = it.row0 + (lane & 31);
+  const int rr = r_row < rows_total ? r_row : rows_total - 1;
+  const int tok = rr / G;
+  const int head = it.kvh * G + (rr - tok * G);
+  const int qpos = pre + tok;
+  const int g_lo = it.kv_begin, g_hi = it.kv_end;
+  const int w_full = min(g_hi, pre + it.row0 / G + 1);      // keys below are visible to all rows
+
+  bf16x8 qop[8];
+  {
+    const uint16_t* qrow = a.q + ((int64_t)(sd.q_start + tok) * a.Hq + head) * kHD;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) qop[ks] = ld_bf16x8(qrow + (2 * ks + hh) * 8);
+  }
+  const int32_t pt_base = ld_uniform(a.indptr + it.seq);
+  const int32_t pt_count = ld_uniform(a.indptr + it.seq + 1) - pt_base;
+  TableCheck tcheck = table_check_issue<P>(a, it, pt_base, pt_count, 64 * kWaves);
+  if constexpr (!kExact) {
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qop[ks][e] = (__bf16)((float)qop[ks][e] * a.c);
+  }
+  const bool table_ok = table_check_finish(a, tcheck, pt_base, 64 * kWaves);
+
+  lds_u8* const vslice[2] = {(wave & 2 ? L.k1 : L.k0) + (wave & 1) * kSliceBytes,
+                             (wave & 2 ? L.v1 : L.v0) + (wave & 1) * kSliceBytes};
+  const int64_t slot_bytes = (int64_t)a.Hkv * P * kHD * 2;
+  const uint32_t pool_bytes = (uint32_t)(a.num_slots * slot_bytes);      // < 2^31 (caller's condition)
+  const __amdgpu_buffer_rsrc_t rsrc_k =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.k), (short)0, (int)pool_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsrc_v =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.v), (short)0, (int)pool_bytes, 0x00020000);
+  const int krow = lane & 31;
+  const int krow_off = (it.kvh * P + krow % P) * (kHD * 2) + hh * 16;   // this lane's K row, d-chunk parity
+  bool bad = false;
+
+  // Slot of page pg of the sequence, or -1 when the table lacks it or it lies
+  // outside the pool (then the page is not read and the error flag is raised).
+  auto slot_of = [&](int pg) __attribute__((always_inline)) {
+    const int32_t s = pg < pt_count ? ld_uniform(a.indices + pt_base + pg) : -1;
+    return (s >= 0 && s < a.num_slots) ? s : -1;
+  };
+  // Every tile issues exactly 8 K loads and 8 V loads, so that "the next
+  // tile's 16 loads may still be outstanding" is an exact wait: a row that must
+  // not be read gets an offset past the pool's buffer resource (the pool spans
+  // < 2^31 bytes), which returns zeros -- into registers or into LDS alike.
+  constexpr uint32_t kOutside = 0x80000000u;
+  // K of tile u into registers: lane l holds key l % 32, d-chunks 2 i + l / 32
+  // (the MFMA's A operand).  Keys past the item's end and absent pages are zeros
+  // (the former are masked; the latter behave as zero rows, and raise the flag).
+  auto load_k = [&](int u, bf16x8* kr) __attribute__((always_inline)) {
+    int32_t sl[kPagesPerTile];
+#pragma unroll
+    for (int p = 0; p < kPagesPerTile; ++p) {
+      sl[p] = slot_of(u * kPagesPerTile + p);
+      bad |= sl[p] < 0 && u * kDecKeys + p * P < g_hi;
+    }
+    const int32_t s = (kPagesPerTile == 2 && krow >= P) ? sl[kPagesPerTile - 1] : sl[0];
+    const bool ok = s >= 0 && u * kDecKeys + krow < g_hi;
+    const uint32_t base = ok ? (uint32_t)s * (uint32_t)slot_bytes + (uint32_t)krow_off : kOutside;
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      kr[i] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rsrc_k, base + i * 32, 0, 0));
+  };
+  // V of tile u into an LDS slice: load j fills rows 4j .. 4j + 3, lane i one
+  // 16-byte chunk of row 4j + i / 16 (XOR-swizzled as the prefill path's).
+  // Keys past the item's end and absent pages are zero rows, which keep the
+  // masked products finite.
+  auto load_v = [&](int u, lds_u8* dst) __attribute__((always_inline)) {
+    const int ts = u * kDecKeys;
+    int32_t sl[kPagesPerTile];
+#pragma unroll
+    for (int p = 0; p < kPagesPerTile; ++p) sl[p] = slot_of(u * kPagesPerTile + p);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int key = 4 * j + (lane >> 4);
+      const int s = sl[(4 * j) / P];
+      const uint32_t off = (uint32_t)((it.kvh * P + key % P) * (kHD * 2) + (((lane & 15) ^ swz_v(key)) << 4));
+      const bool ok = s >= 0 && ts + key < g_hi;
+      __attribute__((address_space(3))) void* d = (__attribute__((address_space(3))) void*)(dst + j * 1024);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc_v, d, 16, ok ? off : kOutside,
+                                               s >= 0 ? (uint32_t)s * (uint32_t)slot_bytes : 0u, 0, 0);
+    }
+  };
+
+  const int tr_g = lane >> 4, tr_s = lane & 15;
+  const int tr_key = 4 * (tr_g >> 1) + (tr_s >> 2);
+  const int tr_d = 16 * (tr_g & 1) + 4 * (tr_s & 3);
+  f32x16 oacc[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) oacc[dt] = f32x16{};
+  float m_used = -INFINITY, msub = 0.f, l = 0.f;
+  bf16x8 kr[8];
+
+  // Issue order: K(u), V(u), V(u + 4); then in the step of tile u, K(u + 4)
+  // once S(u) has read K(u) out of the registers, and V(u + 8) once the PV
+  // product has read V(u) out of its slice.  At the top of the step of tile
+  // u, K(u) and V(u) have landed once at most V(u + 4)'s 8 loads are
+  // outstanding (K(u + 4) is issued later, within the step).
+  const int u0 = g_lo / kDecKeys;
+  const int u1 = (g_hi + kDecKeys - 1) / kDecKeys;
+  int u = u0 + wave;
+  if (u < u1) {
+    load_k(u, kr);
+    load_v(u, vslice[0]);
+  }
+  if (u + kWaves < u1) load_v(u + kWaves, vslice[1]);
+  auto step = [&](auto bc) __attribute__((always_inline)) {
+    constexpr int b = decltype(bc)::value;
+    if (u + kWaves < u1) __builtin_amdgcn_s_waitcnt(0x0078);             // vmcnt(8), lgkmcnt(0)
+    else __builtin_amdgcn_s_waitcnt(0x0070);                             // vmcnt(0), lgkmcnt(0)
+    asm volatile("" ::: "memory");
+    // S^T = K Q^T over the tile's 32 keys (one 32 x 32 block, 8 MFMAs over d)
+    f32x16 S = f32x16{};
+    if constexpr (!kExact) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) S[e] = -msub;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kr[i], qop[i], S, 0, 0, 0);
+    if (u + kWaves < u1) load_k(u + kWaves, kr);
+    // mask keys past the row's own position or the item's end
+    const int ts = u * kDecKeys;
+    if (ts + kDecKeys > w_full) {
+      const int lim = min(qpos, g_hi - 1);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int key = ts + 8 * (e >> 2) + 4 * hh + (e & 3);
+        if (key > lim) S[e] = -INFINITY;
+      }
+    }
+    // offset test (exact scale: whenever the row max grows; folded: past 2^kRescaleLog2)
+    float mx = S[0];
+#pragma unroll
+    for (int e = 1; e < 16; ++e) mx = vmax(mx, S[e]);
+    mx = pair_max(mx);
+    const float cand = kExact ? mx * a.c : mx + msub;
+    if (__ballot(cand > m_used + (kExact ? kRescaleLog2Exact : kRescaleLog2))) {
+      const float m_new = fmaxf(m_used, cand);
+      const float alpha = (m_new == -INFINITY) ? 1.f : exp2f_fast(m_used - m_new);
+      m_used = m_new;
+      const float msub_new = (m_used == -INFINITY) ? 0.f : m_used;
+      const float shift = msub_new - msub;
+      msub = msub_new;
+      l *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) oacc[dt][e] *= alpha;
+      if constexpr (!kExact) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) S[e] -= shift;
+      } else {
+        (void)shift;
+      }
+    }
+    // P = exp2(x), packed to bf16 in the P^T operand order (16-key group g,
+    // slots 2 (j & 3) and 2 (j & 3) + 1 from accumulator 8 g + 2 (j & 3) + h)
+    bf16x8 pop[2];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int g = j >> 2, e = 2 * (j & 3);
+      const float x0 = S[8 * g + e], x1 = S[8 * g + e + 1];
+      const float p0 = kExact ? exp2f_fast(__builtin_fmaf(x0, a.c, -msub)) : exp2f_fast(x0);
+      const float p1 = kExact ? exp2f_fast(__builtin_fmaf(x1, a.c, -msub)) : exp2f_fast(x1);
+      pop[g][e] = (__bf16)p0;
+      pop[g][e + 1] = (__bf16)p1;
+      l += p0 + p1;
+    }
+    // O^T += V^T P^T: 2 groups of 16 keys x 4 blocks of 32 d
+    const lds_u8* const vb = vslice[b];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      bf16x8 vop;
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        const int vkey = 16 * (i >> 2) + 8 * r + tr_key;
+        const int d = 32 * (i & 3) + tr_d;
+        const bf16x4 x = lds_read_tr(vb + vkey * 256 + ((((d >> 3) ^ swz_v(vkey)) << 4) | ((d & 7) << 1)));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) vop[4 * r + e] = x[e];
+      }
+      oacc[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[i >> 2], oacc[i & 3], 0, 0, 0);
+    }
+    __builtin_amdgcn_s_waitcnt(0xC07F);                    // lgkmcnt(0): V operands read out of LDS
+    asm volatile("" ::: "memory");
+    if (u + 2 * kWaves < u1) load_v(u + 2 * kWaves, vslice[b]);
+    u += kWaves;
+  };
+  while (u < u1) {
+    step(IntC<0>{});
+    if (u >= u1) break;
+    step(IntC<1>{});
+  }
+  if (bad && lane == 0) atomicOr(a.err, 1);
+
+  // ---- merge the four waves' partial results through LDS (the tile slices are free)
+  __builtin_amdgcn_s_waitcnt(0x0070);
+  __syncthreads();
+  // wave w > 0 leaves its O^T in one 16 KB array (k0, k1, v0), m and l in v1
+  auto xo = [&](int w) __attribute__((always_inline)) {
+    lds_u8* const x[3] = {L.k0, L.k1, L.v0};
+    return (__attribute__((address_space(3))) float*)x[w];
+  };
+  __attribute__((address_space(3))) float* const xml = (__attribute__((address_space(3))) float*)L.v1;
+  if (wave > 0) {
+    __attribute__((address_space(3))) float* const dst = xo(wave - 1);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int dt = k >> 2, i = k & 3;
+      *(__attribute__((address_space(3))) f32x4*)(dst + (k * 64 + lane) * 4) =
+          f32x4{oacc[dt][4 * i], oacc[dt][4 * i + 1], oacc[dt][4 * i + 2], oacc[dt][4 * i + 3]};
+    }
+    xml[((wave - 1) * 2) * 64 + lane] = m_used;
+    xml[((wave - 1) * 2 + 1) * 64 + lane] = l;
+  }
+  __syncthreads();
+  if (wave > 0) return;
+#pragma unroll
+  for (int w = 0; w < kWaves - 1; ++w) {
+    const float m_b = xml[(w * 2) * 64 + lane];
+    const float l_b = xml[(w * 2 + 1) * 64 + lane];
+    const float m_new = fmaxf(m_used, m_b);
+    const float alpha = (m_used == -INFINITY) ? 0.f : exp2f_fast(m_used - m_new);
+    const float beta = (m_b == -INFINITY) ? 0.f : exp2f_fast(m_b - m_new);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int dt = k >> 2, i = k & 3;
+      const f32x4 ob = *(const __attribute__((address_space(3))) f32x4*)(xo(w) + (k * 64 + lane) * 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) oacc[dt][4 * i + e] = oacc[dt][4 * i + e] * alpha + ob[e] * beta;
+    }
+    l = l * alpha + l_b * beta;
+    m_used = m_new;
+  }
+  const float l_tot = pair_sum(l);
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  const float lse2 = l_tot > 0.f ? m_used + __builtin_amdgcn_logf(l_tot) : -INFINITY;
+  if (it.part < 0) {
+    if (r_row < rows_total) {
+      uint16_t* orow = a.o + ((int64_t)(sd.q_start + tok) * a.Hq + head) * kHD;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int d = 32 * dt + 8 * i + 4 * hh;
+          st_bf16x4(orow + d, oacc[dt][4 * i] * inv, oacc[dt][4 * i + 1] * inv, oacc[dt][4 * i + 2] * inv,
+                    oacc[dt][4 * i + 3] * inv);
+        }
+      if (a.lse != nullptr && hh == 0)
+        a.lse[(int64_t)(sd.q_start + tok) * a.Hq + head] = lse2 * 0.69314718055994531f;
+    }
+  } else {
+    // partial of a key-range part: rows 0 .. 31 of the part's slot
+    float* po = a.part_o + ((int64_t)it.part * kPipeRows + (lane & 31)) * kHD;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int d = 32 * dt + 8 * i + 4 * hh;
+        *(f32x4*)(po + d) = f32x4{oacc[dt][4 * i] * inv, oacc[dt][4 * i + 1] * inv, oacc[dt][4 * i + 2] * inv,
+                                  oacc[dt][4 * i + 3] * inv};
+      }
+    if (hh == 0) a.part_lse[(int64_t)it.part * kPipeRows + (lane & 31)] = lse2;
+  }
+}
+
 // One group of four waves per block, two blocks per CU.
 // kApp: the launch also writes the segment's new K/V rows (app_produce).
 // kExact: the softmax scale is applied in fp32 to each score instead of to
@@ -846,7 +1150,10 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
     const SeqDesc sd{it.q_start, it.q_len, it.kv_len, 0};
     const PipeLds L{(lds_u8*)k_lds0, (lds_u8*)k_lds1, (lds_u8*)v_lds0, (lds_u8*)v_lds1,
                     nullptr, nullptr, nullptr, nullptr, nullptr};
-    pipe_group<P, kPoolRsrc, 1, 0, kApp, kExact>(a, it, sd, L);
+    if (!kApp && kPoolRsrc && it.q_len * a.G <= kDecRows)
+      decode_group<P, kExact>(a, it, sd, L);
+    else
+      pipe_group<P, kPoolRsrc, 1, 0, kApp, kExact>(a, it, sd, L);
   }
   if constexpr (kApp) app_finish(a);
   if (a.blk_clock != nullptr) {

@@ -15,6 +15,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <functional>
 #include <map>
 #include <string>
 #include <vector>
@@ -27,6 +28,10 @@ constexpr int kHD = 128;          // head dim
 constexpr int kKT = 64;           // keys per attention tile
 constexpr int kMaxRows = 256;     // largest query-row tile of a work item
 constexpr int kNumXcd = 8;        // MI355X: 8 accelerator complex dies, 32 CUs each
+// Items of at most this many packed query rows (decode requests: one token,
+// G query heads) take the kernel's decode path, which spreads the item's keys
+// over the block's four waves instead of its rows.
+constexpr int kDecodeRows = 32;
 
 // One attention work item: a tile of packed query rows of one (sequence, KV
 // head) over a key range.
@@ -361,7 +366,7 @@ inline void plan_attn_items(const sa_layout* layout, const std::vector<SeqDesc>&
         const int last = std::min(r0 + rows_item - 1, rows - 1);
         const int kv_end = pre + last / G + 1;
         const int64_t tiles = (kv_end + kKT - 1) / kKT;
-        work.push_back({{b, g, r0, 0, kv_end, -1, 0, 0, 0, 0}, tiles, rows <= 32, (b * Hkv + g) % kNumXcd});
+        work.push_back({{b, g, r0, 0, kv_end, -1, 0, 0, 0, 0}, tiles, rows <= kDecodeRows, (b * Hkv + g) % kNumXcd});
         total_tiles += tiles;
       }
   }
@@ -445,8 +450,34 @@ inline void plan_attn_items(const sa_layout* layout, const std::vector<SeqDesc>&
   // shortest and every CU gets about the same work.  A kernel with one block
   // per CU keeps the longest-first order: each later block goes to the CU
   // that frees first.
-  const bool pair = shape.pair_rounds;
-  auto pair_rounds = [pair](std::vector<AttnItem>& q, size_t first_round) {
+  //
+  // Mixed launches (decode requests beside prefill chunks) are placed so that
+  // every CU holds a decode item and a prefill item from the start: decode
+  // items are bound by HBM and prefill items by the matrix cores, so the two
+  // overlap.  In each queue the first round is decode items, the second
+  // prefill items (their partners), then the remaining decode items -- the
+  // dispatcher gives later blocks the slots that free first, and the decode
+  // items free theirs first -- then the remaining prefill items.
+  bool any_decode = false, any_prefill = false;
+  for (const Work& w : work) (w.decode ? any_decode : any_prefill) = true;
+  const bool mixed = any_decode && any_prefill;
+  auto mix_rounds = [&](std::vector<AttnItem>& q, size_t round) {
+    std::vector<AttnItem> d, p;
+    for (const AttnItem& x : q) ((int64_t)seqs[x.seq].q_len * G <= kDecodeRows ? d : p).push_back(x);
+    if (d.empty() || p.empty()) return;
+    const size_t nd = std::min(d.size(), round), np = std::min(p.size(), round);
+    q.clear();
+    q.insert(q.end(), d.begin(), d.begin() + nd);
+    q.insert(q.end(), p.begin(), p.begin() + np);
+    q.insert(q.end(), d.begin() + nd, d.end());
+    q.insert(q.end(), p.begin() + np, p.end());
+  };
+  const bool pair = shape.pair_rounds && !mixed;
+  auto pair_rounds = [&](std::vector<AttnItem>& q, size_t first_round) {
+    if (mixed) {
+      mix_rounds(q, first_round);
+      return;
+    }
     if (!pair) return;
     if (q.size() > first_round && q.size() <= 2 * first_round) std::reverse(q.begin() + first_round, q.end());
   };
@@ -455,7 +486,7 @@ inline void plan_attn_items(const sa_layout* layout, const std::vector<SeqDesc>&
   if (mx > 0 && (double)(mx - mn) <= 0.1 * (double)mx) {
     std::vector<std::vector<AttnItem>> queue(kNumXcd);
     for (const Work& w : work) queue[w.xcd].push_back(w.it);
-    if (xcd != nullptr && xcd->weighted) {
+    if (xcd != nullptr && xcd->weighted && !mixed) {
       bool same = xcd->in.size() == queue.size();
       for (size_t x = 0; same && x < queue.size(); ++x)
         same = xcd->in[x].size() == queue[x].size() &&
@@ -504,6 +535,35 @@ inline void plan_attn_items(const sa_layout* layout, const std::vector<SeqDesc>&
       items[b].boost = (int32_t)std::lround(std::min(std::max(x, 0.0), l_new));
     }
   }
+}
+
+// Shape of a planned attention launch, for latency models: its workgroups,
+// the key-range parts of split items (a partial-merge launch follows when
+// there are any), its 64-key tiles, and its makespan in tiles when the items
+// are taken in launch order by the first of 2 x num_cu workgroup slots to
+// free (a decode item counts a quarter of its tiles: its four waves split
+// them).
+struct AttnPlanStats {
+  int64_t items = 0, parts = 0, tiles = 0, makespan_tiles = 0;
+};
+
+inline AttnPlanStats attn_plan_stats(const AttnPlan& plan, const std::vector<SeqDesc>& seqs, int G, int num_cu) {
+  AttnPlanStats st;
+  st.items = (int64_t)plan.items.size();
+  st.parts = plan.n_parts;
+  const size_t slots = (size_t)std::max(1, 2 * num_cu);
+  std::vector<int64_t> free_at(slots, 0);          // a min-heap of slot finish times (in tiles x 4)
+  for (const AttnItem& it : plan.items) {
+    if (it.kv_end <= it.kv_begin) continue;
+    const int64_t t = item_tiles(it);
+    st.tiles += t;
+    const int64_t cost = (int64_t)seqs[it.seq].q_len * G <= kDecodeRows ? t : 4 * t;
+    std::pop_heap(free_at.begin(), free_at.end(), std::greater<int64_t>());
+    free_at.back() += cost;
+    std::push_heap(free_at.begin(), free_at.end(), std::greater<int64_t>());
+  }
+  st.makespan_tiles = (*std::max_element(free_at.begin(), free_at.end()) + 3) / 4;
+  return st;
 }
 
 // ------------------------------------------------ debug checks of slot lists

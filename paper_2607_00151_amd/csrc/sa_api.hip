@@ -861,6 +861,29 @@ sa_status sa_segment_prefill_attn(sa_ctx* ctx, const sa_layout* layout, int32_t 
                      h_kv_len, pages, softmax_scale, o, lse, stream);
 }
 
+sa_status sa_attn_plan_stats(const sa_layout* layout, int32_t batch, const int32_t* h_q_len,
+                             const int32_t* h_kv_len, int32_t num_cu, int64_t* out) {
+  std::vector<sa::SeqDesc> seqs;
+  int64_t total_q = 0;
+  sa_status s = sa::plan_attn_check(layout, 0, batch, h_q_len, h_kv_len, 1.f, seqs, total_q, g_err);
+  if (s != SA_OK) return s;
+  if (!out) return fail(SA_ERR_NULL, "out is NULL");
+  if (num_cu < 1) return fail(SA_ERR_SHAPE, "num_cu %d < 1", num_cu);
+  const AttnVariant var = attn_variant();
+  sa::AttnShape shape;
+  shape.rows_item = 32 * var.qt * var.waves;
+  shape.num_cu = num_cu;
+  shape.pair_rounds = var.pipe != 2;
+  sa::AttnPlan plan;
+  sa::plan_attn_items(layout, seqs, shape, nullptr, plan);
+  const sa::AttnPlanStats st = sa::attn_plan_stats(plan, seqs, layout->num_q_heads / layout->num_kv_heads, num_cu);
+  out[0] = st.items;
+  out[1] = st.parts;
+  out[2] = st.tiles;
+  out[3] = st.makespan_tiles;
+  return SA_OK;
+}
+
 sa_status sa_segment_prefill_attn_noalloc(sa_ctx* ctx, const sa_layout* layout, int32_t layer,
                                           const void* q, const void* k_pool, const void* v_pool,
                                           int32_t batch, const int32_t* h_q_len, const int32_t* h_kv_len,

@@ -33,11 +33,14 @@ class Item:
     kv: int            # KV length once the unit has run (prefix + q)
 
 
-def est_batch_latency(coef, batch) -> float:
-    """Eq. 1 without the GEMM term: c + alpha_d * sum L_j + alpha_p * sum A_j (ms)."""
+def est_batch_latency(coef, batch, layout=None) -> float:
+    """Eq. 1 without the GEMM term: c + alpha_d * sum L_j + alpha_p * sum A_j (ms); with a
+    layout and the five coefficients of the launch-shape model, also its two launch-shape
+    terms, taken from the library's planner for this batch."""
     if not batch:
         return 0.0
-    return float(pm.predict_context(coef, [pm.features([x.q for x in batch], [x.kv for x in batch])])[0])
+    w = pm.features([x.q for x in batch], [x.kv for x in batch], layout if len(coef) == 5 else None)
+    return float((pm.predict_shape if len(coef) == 5 else pm.predict_context)(coef, [w])[0])
 
 
 def hybrid_batch(dec_q, lc_q, be_q, delta, est):
@@ -107,19 +110,20 @@ def run(out_path=None, iters=24, delta_ms=0.4, be_loads=(0, 2, 4, 8, 16), n_deco
     import paper_2607_00151_amd as sa
 
     P, Hq, Hkv, D = 16, 32, 8, 128
-    # coefficients of the latency model, profiled on this kernel first: fitted on
-    # every launch of the model sweep (decode-only, prefill-only and mixed batches)
+    # coefficients of the latency model (Eq. 1's attention terms and the launch
+    # shape), profiled on this kernel first: fitted on every launch of the model
+    # sweep (decode-only, prefill-only and mixed batches)
     prof = pm.run()
     launches = prof["profile"] + prof["mixed"]
-    coef = pm.fit_context_model([pm.Work(x["tokens"], x["decode_keys"], x["prefill_pairs"]) for x in launches],
-                                [x["ms"] for x in launches])
-    est = lambda b: est_batch_latency(coef, b)   # noqa: E731
+    coef = pm.fit_shape_model([pm.Work(x["tokens"], x["decode_keys"], x["prefill_pairs"], x["excess_tiles"],
+                                       x["split"]) for x in launches], [x["ms"] for x in launches])
 
     max_kv = 16384 + iters + 1 + 16384 + 2048 + 4096
     pages_per_req = (max_kv + P - 1) // P
     n_req = n_decode + n_lc + max(be_loads)
     L = sa.Layout(num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D, page_size=P, num_layers=1,
                   num_slots=pages_per_req * (n_req + 4))
+    est = lambda b: est_batch_latency(coef, b, L)   # noqa: E731
     g = torch.Generator(device="cuda").manual_seed(3)
     shape = (L.num_slots, Hkv, P, D)
     pools = [(torch.randn(shape, generator=g, device="cuda") * 0.5).to(torch.bfloat16).view(torch.int16)
@@ -128,7 +132,8 @@ def run(out_path=None, iters=24, delta_ms=0.4, be_loads=(0, 2, 4, 8, 16), n_deco
     q_all = (torch.randn((n_decode + 64 * 256, Hq, D), generator=g, device="cuda") * 0.5).to(torch.bfloat16)
     o_all = torch.empty_like(q_all)
     stream = torch.cuda.current_stream()
-    rec = {"delta_ms": delta_ms, "model": {"c_ms": coef[0], "alpha_d": coef[1], "alpha_p": coef[2]},
+    rec = {"delta_ms": delta_ms, "model": {"c_ms": coef[0], "alpha_d": coef[1], "alpha_p": coef[2],
+                                           "beta_excess_tile": coef[3], "gamma_split": coef[4]},
            "runs": []}
 
     with sa.Context(0) as ctx:

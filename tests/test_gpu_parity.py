@@ -514,6 +514,8 @@ def check_step(ctx, w, per_seq_rows, mode="copy", folded=False):
     lse = torch.empty((T, w.num_q_heads), dtype=torch.float32, device="cuda")
     state = (kp, vp, sip, sid, fresh, dip, did, dev_u16(w.q), dev_u16(w.k_seg()),
              dev_u16(w.v_seg()), o, lse)
+    if not alias:
+        pools_before = (kp.clone(), vp.clone())
     dst_len = run_step(ctx, w, L, state, mode)
     sa.sa_sync_check(ctx)
     assert np.array_equal(dst_len, w.pre)
@@ -531,8 +533,25 @@ def check_step(ctx, w, per_seq_rows, mode="copy", folded=False):
             assert torch.equal(after[0][keep], before[0][keep])
     assert np.array_equal(dip.cpu().numpy(), r["dst_indptr"])
     assert np.array_equal(did.cpu().numpy()[: r["dst_indptr"][-1]], r["dst_indices"])
+    if not alias:
+        # the whole pools, every slot and row: the oracle's splice (surviving pages copied
+        # whole to their fresh slots) then its append, applied to the pools as they were;
+        # canary-filled slots nobody writes must come out unchanged
+        sl, ro = opages.append_destinations(r["dst_len"], w.qlen, r["dst_indptr"], r["dst_indices"],
+                                            w.page_size)
+        csrc = torch.from_numpy(np.asarray(r["copy_src"], dtype=np.int64)).cuda()
+        cdst = torch.from_numpy(np.asarray(r["copy_dst"], dtype=np.int64)).cuda()
+        for after, before, seg in ((kp, pools_before[0], w.k_seg()), (vp, pools_before[1], w.v_seg())):
+            want = before.clone()
+            want[0, cdst] = before[0, csrc]
+            if len(sl):
+                view = want[0].permute(0, 2, 1, 3)                  # [slot][row][head][d]
+                view[torch.from_numpy(sl).cuda(), torch.from_numpy(ro).cuda()] = dev_u16(seg)
+            assert torch.equal(after, want)
+            del want
+        del pools_before
     ip_h, ix_h = r["dst_indptr"], r["dst_indices"]
-    for b in sorted({0, w.batch - 1}):
+    for b in range(w.batch):
         pages_b = ix_h[ip_h[b]: ip_h[b + 1]]
         kv_b = int(w.kv[b])
         for pool, full in ((kp, w.k), (vp, w.v)):
@@ -773,7 +792,7 @@ def test_step_c2_full_fused(ctx, mode):
 @pytest.mark.timeout(900)
 def test_step_c3_full(ctx):
     print("c3 full step", flush=True)
-    check_step(ctx, workloads.make("c3"), per_seq_rows=48)
+    check_step(ctx, workloads.make("c3"), per_seq_rows=192)
 
 
 def check_direct(ctx, w, per_seq_rows, extra_rows=None, fused=False, folded=False):
@@ -817,11 +836,11 @@ def test_c4_full_outliers(ctx):
     sel = (out_tok >= 0) & (out_tok < int(w.qlen[0]))
     G = w.num_q_heads // w.num_kv_heads
     extra = (out_tok[sel][:64].astype(np.int64), (out_kvh[sel][:64] * G).astype(np.int32))
-    check_direct(ctx, w, per_seq_rows=160, extra_rows=extra)
+    check_direct(ctx, w, per_seq_rows=640, extra_rows=extra)
 
 
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("fused", [False, True])
 def test_c5_full_mixed(ctx, fused):
     print(f"c5 full, append inside attention {fused}", flush=True)
-    check_direct(ctx, workloads.make("c5"), per_seq_rows=24, fused=fused)
+    check_direct(ctx, workloads.make("c5"), per_seq_rows=96, fused=fused)

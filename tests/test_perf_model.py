@@ -68,3 +68,37 @@ def test_segment_roofline_bound_switches_at_the_ridge():
         got = "hbm" if byt / (sg.PEAK_GBS * 1e9) > flop / (sg.PEAK_TFLOPS * 1e12) else "mfma"
         assert got == bound, q
         assert abs(flop - 4 * 128 * 32 * 32 * pm.prefill_pairs(q, 8192)) < 1e-3 * flop
+
+
+def _layout():
+    import paper_2607_00151_amd as sa
+    return sa.Layout(num_q_heads=32, num_kv_heads=8, head_dim=128, page_size=16, num_layers=1, num_slots=1 << 20)
+
+
+def test_launch_shape_terms_come_from_the_planner():
+    """The planner's own view of a launch (host only): a single short segment underfills
+    the slots (makespan far above an even spread, no split); a few long decode requests
+    are split by key range; the c2 shape fills one round whose longest item outlasts the
+    mean (the causal imbalance)."""
+    import paper_2607_00151_amd as sa
+    L = _layout()
+    st = sa.sa_attn_plan_stats(L, [2048], [8192 + 2048])
+    assert st["items"] == 512 and st["parts"] == 0
+    # 8 KV heads x 64 row tiles of 32 tokens; tile k sees 8192 + 32 (k + 1) keys
+    assert st["tiles"] == 8 * sum(-(-(8192 + 32 * (k + 1)) // 64) for k in range(64))
+    assert st["makespan_tiles"] == (8192 + 2048) // 64            # the longest row tile
+    w = pm.features([2048], [10240], L)
+    assert abs(w.excess_tiles - (160 - st["tiles"] / 512)) < 1e-9 and w.split == 0
+    w = pm.features([1] * 4, [32768] * 4, L)
+    assert w.split == 1
+    w = pm.features([256], [256], L)
+    assert w.excess_tiles > 0 and w.split == 0
+
+
+def test_shape_fit_recovers_known_coefficients():
+    L = _layout()
+    coef = (0.012, 3.0e-8, 2.5e-10, 4.0e-4, 0.009)
+    works = [pm.features(qs, kvs, L) for _, qs, kvs in pm.profiling_batches()]
+    t = pm.predict_shape(coef, works)
+    got = pm.fit_shape_model(works, t)
+    assert np.allclose(got, coef, rtol=1e-6, atol=1e-12)
