@@ -64,6 +64,11 @@ def parse():
     p.add_argument("--config", choices=("c1", "c2", "c3", "c4", "c5"), default="c2",
                    help="workload; c2 is the benchmark line, the others are measured the same way "
                         "(splice where the configuration has one, append, attention) without rotation")
+    p.add_argument("--assemble-only", choices=("shuffled", "contiguous"), default=None,
+                   help="time only the c2 commit splice over --assemble-layers layers, on the shuffled page "
+                        "placement of the workload or on an identity placement (surviving pages and fresh "
+                        "slots each one contiguous run): the same kernel and bytes, with and without the "
+                        "address spread")
     p.add_argument("--copy-bytes", type=int, default=0,
                    help="instead of the step, time a plain device copy of this many bytes "
                         "(calibrates the FETCH_SIZE / WRITE_SIZE counters)")
@@ -220,6 +225,59 @@ def copy_mode(nbytes: int, steps: int, warmup: int):
     ms = a.elapsed_time(b) / steps
     print(json.dumps({"mode": "copy", "bytes_read": 2 * n, "bytes_written": 2 * n,
                       "ms": ms, "gbs": 4 * n / (ms * 1e-3) / 1e9}), flush=True)
+
+
+def assemble_mode(args):
+    """The c2 commit splice of every layer in one launch, timed by kernel events, on
+    the workload's shuffled page placement or on a contiguous one."""
+    import torch
+    import paper_2607_00151_amd as sa
+    import workloads
+    w = workloads.make("c2")
+    a = w.asm
+    NL, Hkv, P = max(1, args.assemble_layers), w.num_kv_heads, w.page_size
+    n_src = int(a.src_indptr[-1])
+    if args.assemble_only == "contiguous":
+        src_ix = np.arange(n_src, dtype=np.int32)
+        fresh = np.arange(n_src, n_src + len(a.fresh), dtype=np.int32)
+        slots = n_src + len(a.fresh)
+    else:
+        src_ix, fresh, slots = a.src_indices, a.fresh, w.num_slots
+    L = sa.Layout(num_q_heads=w.num_q_heads, num_kv_heads=Hkv, head_dim=128, page_size=P, num_layers=NL,
+                  num_slots=slots)
+    kl = torch.zeros((NL, slots, Hkv, P, 128), dtype=torch.int16, device="cuda")
+    vl = torch.zeros_like(kl)
+    sip, sid, fr = dev_i32(a.src_indptr), dev_i32(src_ix), dev_i32(fresh)
+    dip = torch.zeros(w.batch + 1, dtype=torch.int32, device="cuda")
+    did = torch.zeros(len(a.fresh), dtype=torch.int32, device="cuda")
+    ctx = sa.Context(0)
+    stream = torch.cuda.current_stream()
+
+    def run():
+        sa.sa_kv_assemble(ctx, L, kl, vl, kl, vl, a.src_len, a.keep_indptr, a.keep_spans, a.reserve, sip, sid,
+                          fr, dip, did)
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    for e in ev:
+        e[0].record(stream)
+        e[1].record(stream)
+    torch.cuda.synchronize()
+    for e in ev:
+        sa.sa_set_kernel_events(ctx, sa.TIMED_PAGES, e[0].cuda_event, e[1].cuda_event)
+        run()
+    sa.sa_set_kernel_events(ctx, sa.TIMED_PAGES)
+    torch.cuda.synchronize()
+    sa.sa_sync_check(ctx)
+    ms = float(np.median([e[0].elapsed_time(e[1]) for e in ev]))
+    kept_pages = int(sum(e - b for b, e in a.keep_spans))
+    n_dst = int(sum(-(-int(x + y) // P) for x, y in zip(w.pre, w.qlen)))
+    nbytes = 2 * kept_pages * 2 * Hkv * P * 128 * 2 * NL + 4 * (n_dst + kept_pages + w.batch + 1)
+    ctx.close()
+    print(json.dumps({"mode": "assemble", "placement": args.assemble_only, "layers": NL, "pages": kept_pages,
+                      "bytes": nbytes, "ms": ms, "gbs": nbytes / (ms * 1e-3) / 1e9,
+                      "frac_of_hbm": nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS}), flush=True)
 
 
 def config_mode(args):
@@ -414,6 +472,9 @@ def main():
         sys.exit(2)
     if args.copy_bytes:
         copy_mode(args.copy_bytes, args.steps, args.warmup)
+        return
+    if args.assemble_only:
+        assemble_mode(args)
         return
     if args.config != "c2":
         config_mode(args)
