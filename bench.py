@@ -10,9 +10,10 @@ One step = splice, append of the segment's K/V, attention, all on the current
 stream with inputs resident in HBM.  --fuse picks the entry points:
 "splice" (default): sa_kv_assemble_append (splice and append in one launch)
 -> sa_segment_prefill_attn; "attn": sa_kv_assemble ->
-sa_segment_prefill_attn_append (two launches, or one for the append and the
-attention together with SA_APPEND_IN_ATTN=1); "none": sa_kv_assemble ->
-sa_kv_append -> sa_segment_prefill_attn.  Every step uses one of R
+sa_segment_prefill_attn_append with sa_set_fused_append on (the attention
+launch writes the segment's rows and reads the segment's keys from k_new /
+v_new); "none": sa_kv_assemble
+-> sa_kv_append -> sa_segment_prefill_attn.  Every step uses one of R
 disjoint copies of the cache (default 8 x 128 MB per pool), so the 256 MB
 Infinity Cache cannot hold the data a step reads from its previous use.
 
@@ -497,6 +498,8 @@ def main():
     ctx = sa.Context(0)
     if args.folded_scale:
         sa.sa_set_exact_scale(ctx, False)
+    if args.fuse == "attn":
+        sa.sa_set_fused_append(ctx, True)
     kp, vp = new_pool(base_slots * R, w.num_kv_heads, w.page_size), new_pool(base_slots * R, w.num_kv_heads,
                                                                               w.page_size)
     copies = []
@@ -515,10 +518,14 @@ def main():
     stream = torch.cuda.current_stream()
     fuse = args.fuse
 
-    def step(r, ev=None):
+    def step(r, ev=None, pages_ev=None):
+        """One step; ev: four events recorded around the calls; pages_ev: kernel
+        events for the step's first page kernel and (fuse "none") the append."""
         c = copies[r % R]
         if ev is not None:
             ev[0].record(stream)
+        if pages_ev is not None:
+            sa.sa_set_kernel_events(ctx, sa.TIMED_PAGES, pages_ev[0][0].cuda_event, pages_ev[0][1].cuda_event)
         if fuse == "splice":
             kept = sa.sa_kv_assemble_append(ctx, L, kp, vp, kp, vp, a.src_len, a.keep_indptr,
                                             a.keep_spans, a.reserve, c["sip"], c["sid"], c["fresh"],
@@ -531,6 +538,9 @@ def main():
             if ev is not None:
                 ev[1].record(stream)
             if fuse == "none":
+                if pages_ev is not None:
+                    sa.sa_set_kernel_events(ctx, sa.TIMED_PAGES, pages_ev[1][0].cuda_event,
+                                            pages_ev[1][1].cuda_event)
                 sa.sa_kv_append(ctx, L, 0, kp, vp, ks, vs, kept, w.qlen, c["dip"], c["did"])
         if ev is not None:
             ev[2].record(stream)
@@ -591,11 +601,8 @@ def main():
     # time their execution on the device; recorded once here so that the HIP
     # events exist
     kev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(K)]
-    pev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(K)]
-    for e in pev:
-        e[0].record(stream)
-        e[1].record(stream)
-    for e in kev:
+    pev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(2)] for _ in range(K)]
+    for e in [x for p in pev for x in p] + kev:
         e[0].record(stream)
         e[1].record(stream)
     torch.cuda.synchronize()
@@ -604,9 +611,7 @@ def main():
     ev_start.record(stream)
     for i in range(K):
         sa.sa_set_kernel_events(ctx, sa.TIMED_ATTN, kev[i][0].cuda_event, kev[i][1].cuda_event)
-        if fuse == "splice":
-            sa.sa_set_kernel_events(ctx, sa.TIMED_PAGES, pev[i][0].cuda_event, pev[i][1].cuda_event)
-        step(args.warmup + K + i, evs[i])
+        step(args.warmup + K + i, evs[i], pev[i])
     sa.sa_set_kernel_events(ctx, sa.TIMED_ATTN)
     sa.sa_set_kernel_events(ctx, sa.TIMED_PAGES)
     ev_end.record(stream)
@@ -676,28 +681,30 @@ def main():
     if not args.no_gemm_reference:
         rec["gemm_reference"] = gemm_reference()
 
-    in_attn = fuse == "attn" and os.environ.get("SA_APPEND_IN_ATTN") == "1"
-    rec["config"]["launches"] = {"attn": "splice | append + attention" if in_attn else
-                                 "splice | append | attention (sa_segment_prefill_attn_append)",
+    rec["config"]["launches"] = {"attn": "splice | append + attention (one launch, segment rows read from k_new/v_new)",
                                  "splice": "splice + append | attention",
                                  "none": "splice | append | attention"}[fuse]
+    # each page kernel's own time (kernel events)
+    first_ms = float(np.mean([p[0][0].elapsed_time(p[0][1]) for p in pev]))
+    kernels_ms = first_ms + attn_ms
     if fuse == "splice":
-        # the splice + append kernel's own time (kernel events), and the call's
-        sp_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in pev]))
         sp_bytes = asm_bytes + app_bytes
-        rec["splice_append"] = {"ms": sp_ms, "timing": "kernel events (hipExtLaunchKernelGGL)",
+        rec["splice_append"] = {"ms": first_ms, "timing": "kernel events (hipExtLaunchKernelGGL)",
                                 "call_ms": asm_ms + app_ms, "bytes": sp_bytes,
-                                "gbs": sp_bytes / (sp_ms * 1e-3) / 1e9,
-                                "frac_of_hbm": sp_bytes / (sp_ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
-    elif fuse == "attn":
-        rec["assemble"] = {"ms": asm_ms + app_ms, "bytes": asm_bytes,
-                           "gbs": asm_bytes / ((asm_ms + app_ms) * 1e-3) / 1e9,
-                           "frac_of_hbm": asm_bytes / ((asm_ms + app_ms) * 1e-3) / 1e9 / PEAK_HBM_GBS}
-        rec["attn"]["includes_append_bytes"] = app_bytes
+                                "gbs": sp_bytes / (first_ms * 1e-3) / 1e9,
+                                "frac_of_hbm": sp_bytes / (first_ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
     else:
-        rec["assemble"] = {"ms": asm_ms, "bytes": asm_bytes, "gbs": asm_bytes / (asm_ms * 1e-3) / 1e9,
-                           "frac_of_hbm": asm_bytes / (asm_ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
-        rec["append"] = {"ms": app_ms, "bytes": app_bytes, "gbs": app_bytes / (app_ms * 1e-3) / 1e9}
+        rec["assemble"] = {"ms": first_ms, "timing": "kernel events (hipExtLaunchKernelGGL)",
+                           "call_ms": asm_ms, "bytes": asm_bytes, "gbs": asm_bytes / (first_ms * 1e-3) / 1e9,
+                           "frac_of_hbm": asm_bytes / (first_ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
+    if fuse == "attn":
+        rec["attn"]["includes_append"] = {"bytes_written": app_bytes // 2}
+    if fuse == "none":
+        ap_ms = float(np.mean([p[1][0].elapsed_time(p[1][1]) for p in pev]))
+        kernels_ms += ap_ms
+        rec["append"] = {"ms": ap_ms, "timing": "kernel events (hipExtLaunchKernelGGL)", "call_ms": app_ms,
+                         "bytes": app_bytes, "gbs": app_bytes / (ap_ms * 1e-3) / 1e9}
+    rec["kernels_ms_per_step"] = kernels_ms
 
     # where the attention launch's time goes across the chip: each workgroup's
     # start and end on the device clock (sa_set_block_clock), over 10 launches;

@@ -336,6 +336,18 @@ sa_status sa_segment_prefill_attn_noalloc(sa_ctx *ctx, const sa_layout *layout, 
 sa_status sa_set_exact_scale(sa_ctx *ctx, int32_t enable);
 
 /*
+ * sa_set_fused_append — how later sa_segment_prefill_attn_append calls on
+ * this context write the segment's rows.  enable != 0: inside the attention
+ * launch, which reads the segment's keys from k_new / v_new; enable == 0 (the
+ * default): an append launch (sa_kv_append) and then the attention.  Both
+ * forms leave the same pool; their outputs are equal bit for bit when every
+ * prefix length is a multiple of 4 and no request has at most 32 query rows,
+ * and otherwise both are held to the same tolerance.
+ * Errors: SA_ERR_NULL for a NULL context.
+ */
+sa_status sa_set_fused_append(sa_ctx *ctx, int32_t enable);
+
+/*
  * sa_set_kernel_events — timing hook for measurement.  While set for `which`,
  * every kernel of that kind this context launches is launched by
  * hipExtLaunchKernelGGL with start_event and stop_event (hipEvent_t handles
@@ -406,13 +418,18 @@ sa_status sa_set_xcd_weights(sa_ctx *ctx, const float *h_speed);
  * k_new / v_new: bf16 [sum h_q_len][num_kv_heads][head_dim], token-major like
  * q; the pools are written.  The pages for the new rows must already be in
  * the table (sa_kv_assemble's reserve).  By default this is the append
- * kernel followed by the attention kernel on `stream`.  With the environment
- * variable SA_APPEND_IN_ATTN=1 (read once per process) and the default
- * attention kernel, the attention launch writes the rows itself: its blocks
- * take the rows from a counter, publish them at device scope, and each wave
- * waits for them only before its first tile holding a new key.  That form
- * coordinates through counters held by the context, so its calls on one
- * context must not overlap in time (for example on two streams at once).
+ * kernel followed by the attention kernel on `stream`.  With fusion switched
+ * on (sa_set_fused_append) it is one launch of the default attention kernel:
+ * every workgroup reads the segment's keys and values from k_new / v_new, not
+ * from their pages, and the first key-range part of each 128-row tile writes
+ * the rows of the tokens whose first query row lies in that tile, so the rows
+ * are written once and no workgroup waits on another (a request of at most
+ * 32 query rows writes its own rows and reads them back).  The fused form
+ * falls back to the two launches for the other kernel variants
+ * (SA_ATTN_VARIANT), when a layer's pool spans 2^31 bytes or more, or when
+ * k_new does.  The rows written must not be
+ * rows that another sequence of the call reads as part of its prefix (as with
+ * the two launches, whose order would otherwise decide what it reads).
  *
  * Errors: those of sa_segment_prefill_attn; SA_ERR_NULL for NULL new rows
  * (when any q_len > 0), SA_ERR_ALIGN for new rows not 16-byte aligned.  A

@@ -15,8 +15,8 @@ import numpy as np
 __all__ = [
     "Layout", "Context", "SaError", "library_path", "load_library",
     "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append", "sa_kv_splice_alias",
-    "sa_segment_prefill_attn", "sa_segment_prefill_attn_append", "sa_set_exact_scale", "sa_set_kernel_events",
-    "sa_set_block_clock", "sa_set_xcd_weights", "sa_sync_check", "sa_reserve",
+    "sa_segment_prefill_attn", "sa_segment_prefill_attn_append", "sa_set_exact_scale", "sa_set_fused_append",
+    "sa_set_kernel_events", "sa_set_block_clock", "sa_set_xcd_weights", "sa_sync_check", "sa_reserve",
     "sa_segment_prefill_attn_noalloc", "sa_attn_plan_stats", "EXPORTED_SYMBOLS",
 ]
 
@@ -27,9 +27,9 @@ _lib = None
 EXPORTED_SYMBOLS = ("sa_create", "sa_destroy", "sa_status_string", "sa_last_error",
                     "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
                     "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append",
-                    "sa_set_exact_scale", "sa_set_kernel_events", "sa_set_block_clock",
-                    "sa_set_xcd_weights", "sa_reserve", "sa_segment_prefill_attn_noalloc",
-                    "sa_attn_plan_stats")
+                    "sa_set_exact_scale", "sa_set_fused_append", "sa_set_kernel_events",
+                    "sa_set_block_clock", "sa_set_xcd_weights", "sa_reserve",
+                    "sa_segment_prefill_attn_noalloc", "sa_attn_plan_stats")
 
 STATUS = {0: "SA_OK", 1: "SA_ERR_NULL", 2: "SA_ERR_SHAPE", 3: "SA_ERR_UNSUPPORTED",
           4: "SA_ERR_ALIGN", 5: "SA_ERR_RANGE", 6: "SA_ERR_NO_PAGES", 7: "SA_ERR_HIP",
@@ -86,6 +86,7 @@ def load_library():
     lib.sa_segment_prefill_attn_append.argtypes = [P, LP, I32, P, P, P, P, P, I32, P, P, _Pages,
                                                    ctypes.c_float, P, P, P]
     lib.sa_set_exact_scale.argtypes = [P, I32]
+    lib.sa_set_fused_append.argtypes = [P, I32]
     lib.sa_set_kernel_events.argtypes = [P, I32, P, P]
     lib.sa_set_block_clock.argtypes = [P, P, I64, ctypes.POINTER(ctypes.c_int64)]
     lib.sa_set_xcd_weights.argtypes = [P, P]
@@ -94,7 +95,8 @@ def load_library():
     lib.sa_attn_plan_stats.argtypes = [LP, I32, P, P, I32, P]
     for name in ("sa_create", "sa_sync_check", "sa_kv_append", "sa_kv_assemble", "sa_kv_assemble_append",
                  "sa_kv_splice_alias", "sa_segment_prefill_attn", "sa_segment_prefill_attn_append",
-                 "sa_set_exact_scale", "sa_set_kernel_events", "sa_set_block_clock", "sa_set_xcd_weights",
+                 "sa_set_exact_scale", "sa_set_fused_append", "sa_set_kernel_events", "sa_set_block_clock",
+                 "sa_set_xcd_weights",
                  "sa_reserve", "sa_segment_prefill_attn_noalloc", "sa_attn_plan_stats"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
@@ -362,8 +364,15 @@ def sa_segment_prefill_attn_noalloc(ctx, layout: Layout, layer: int, q, k_pool, 
 
 def sa_set_exact_scale(ctx, enable: bool = True):
     """Later attention calls on ctx apply the softmax scale to each score in fp32
-    (enable) or fold it into the bf16 query rows (the default)."""
+    (enable, the default) or fold it into the bf16 query rows."""
     _check(load_library().sa_set_exact_scale(_ctx_handle(ctx), int(bool(enable))))
+
+
+def sa_set_fused_append(ctx, enable: bool = True):
+    """Later sa_segment_prefill_attn_append calls on ctx write the segment's rows
+    inside the attention launch (enable) or with an append launch before it (the
+    default)."""
+    _check(load_library().sa_set_fused_append(_ctx_handle(ctx), int(bool(enable))))
 
 
 def sa_set_block_clock(ctx, buf=None) -> int:

@@ -56,15 +56,12 @@ struct AttnArgs {
   int32_t n_items;
   int32_t Hq, Hkv, G;
   float c;                  // softmax_scale * log2(e)
-  // The segment's own K/V rows, written to their pages by the same launch
-  // (attn_pipe_kernel only; app_tickets == 0: none).
+  // The segment's own K/V rows (attn_pipe_kernel with kRead only): blocks
+  // read the segment's keys from here instead of from their pages, and the
+  // first key-range part of each row tile writes its tokens' rows to the pages.
   const uint16_t* k_new;    // [sum q_len][Hkv][kHD], token-major like q
   const uint16_t* v_new;
-  uint32_t* sync;           // three counters kSyncStride words apart: tickets taken,
-                            // tickets written, blocks finished (zero between launches)
-  int64_t app_chunks;       // sum q_len * Hkv * 16: 16-byte chunks of K (and of V)
-  int32_t app_tickets;      // 64 ceil(app_chunks / (64 kAppTicket))
-  int32_t B;                // sequences in seqs
+  uint32_t new_bytes;       // bytes of each of k_new, v_new (< 2^31)
   // nullable (attn_pipe_kernel only): per block {start, end} of the device's
   // constant-rate clock and the item's {sequence, q_len}, four words per block
   uint64_t* blk_clock;

@@ -42,6 +42,19 @@ struct IntC {
   static constexpr int value = N;
 };
 
+// The phase-2 exponentials of the interleaved step go to PV slots
+// ((e - 8 kG1) w2) / (32 - 8 kG1) - 1 and each pair is packed one slot after
+// its second element; the PV MFMAs of 16-key group g are slots 4g .. 4g + 3.
+// True if every group of phase 2 is packed before slot 4g - 1.
+constexpr bool phase2_in_time(int kg1, int w2) {
+  for (int g = kg1; g < 4; ++g) {
+    const int e = 8 * g + 7;                                 // last element of the group
+    const int pack = ((e - 8 * kg1) * w2) / (32 - 8 * kg1);
+    if (pack >= 4 * g - 1) return false;
+  }
+  return true;
+}
+
 constexpr int kPipeWaves = 4;                              // waves per group, 32 rows each
 constexpr int kPipeRows = 32 * kPipeWaves;                 // query rows per work item
 constexpr int kTileBytes = kKT * kHD * 2;                  // one K or V tile, 16 KB
@@ -92,112 +105,56 @@ __device__ __forceinline__ bool table_check_finish(const AttnArgs& a, TableCheck
   return !__syncthreads_or(bad);
 }
 
-// ---- the segment's append inside the attention launch
+// ---- the segment's rows, written by the launch that attends over them
 //
-// Every lane takes tickets from a counter (kAppTicket 16-byte chunks of K and
-// as many of V each, so that few waves hold any) until none is left, writes its chunks to their pages and
-// counts each ticket written.  A wave waits for that count to reach every
-// ticket only before it loads its first tile holding a new key (with a long
-// cached prefix, long after the writes are done).  No lane waits before it has
-// seen every ticket taken, and a lane holding a ticket finishes it without
-// waiting on anything, so every wait ends whatever number of blocks the chip
-// holds at once; a wait is still bounded (kAppSpinLimit polls, then the error
-// flag).  The ticket loop holds no barrier and no cross-lane operation, so it
-// stays correct however the compiler splits its lanes; the compiler merges
-// the lanes' counter updates into one atomic per wave.  The last block to
-// finish zeroes the counters for the next launch.  Ordering: each wave
-// releases its page writes at device scope before it counts them, and a
-// waiting wave acquires at device scope once it sees the full count, so its
-// tile loads read the new rows whichever XCD's L2 wrote them.
-constexpr int kAppTicket = 16;               // chunks of K (and of V) per ticket, a multiple of 4
-constexpr int kSyncStride = 64;              // counters 256 bytes apart
-constexpr int kAppSpinLimit = 1 << 20;       // polls of at least ~0.3 us each
-
-// Largest b with seqs[b].q_start <= t (q_start is non-decreasing).
-__device__ __forceinline__ int seq_of_token(const SeqDesc* seqs, int B, int t) {
-  int lo = 0, hi = B - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (seqs[mid].q_start <= t) lo = mid; else hi = mid - 1;
-  }
-  return lo;
-}
-
+// With kRead every block takes the segment's keys (positions kv_len - q_len
+// on) from the token-major k_new / v_new and never from their pages, so no
+// block depends on another block's writes.  The first key-range part of each
+// row tile (kv_begin == 0) stores to the pages the rows of the tokens whose
+// first query row lies in its tile: the row tiles partition the rows, so every
+// token's row is written exactly once.  A row whose page is missing or lies
+// outside the pool is not written and raises error flag 2, as the append
+// kernel does.  Four chunks per thread are loaded before any is stored, so the
+// block waits for one round trip per 1024 chunks (64 tokens).
 template <int P>
-__device__ __forceinline__ void app_produce(const AttnArgs& a) {
-  const int per_tok = a.Hkv * 16;
+__device__ __forceinline__ void write_own_rows(const AttnArgs& a, const AttnItem& it) {
+  const int G = a.G;
+  const int tb = (it.row0 + G - 1) / G;
+  const int te = min((it.row0 + kPipeRows + G - 1) / G, it.q_len);
+  const int n = (te - tb) * 16;                             // 16-byte chunks of K (and of V)
+  const int pre = it.kv_len - it.q_len;
+  const int32_t pt_base = ld_uniform(a.indptr + it.seq);
+  const int32_t pt_count = ld_uniform(a.indptr + it.seq + 1) - pt_base;
   uint16_t* const kp = const_cast<uint16_t*>(a.k);
   uint16_t* const vp = const_cast<uint16_t*>(a.v);
-  for (;;) {
-    const uint32_t tk = __hip_atomic_fetch_add(a.sync, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (tk >= (uint32_t)a.app_tickets) break;
-    // ticket tk: chunks ((tk / 64) kAppTicket + j) 64 + tk % 64, so the lanes
-    // of a wave, which draw consecutive tickets, read and write consecutive chunks
-    const int64_t c0 = (int64_t)(tk >> 6) * kAppTicket * 64 + (tk & 63);
+  constexpr int kDepth = 4;
+  for (int c0 = (int)threadIdx.x; c0 < n; c0 += kDepth * (int)blockDim.x) {
+    int64_t dst[kDepth];
+    u32x4 kx[kDepth], vx[kDepth];
 #pragma unroll
-    for (int r = 0; r < kAppTicket; r += 4) {
-      int64_t src[4], dst[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int64_t c = c0 + (int64_t)(r + j) * 64;
-        src[j] = -1;
-        if (c >= a.app_chunks) continue;
-        const int t = (int)(c / per_tok);
-        const int rem = (int)(c - (int64_t)t * per_tok);
-        const int g = rem >> 4, ch = rem & 15;
-        const int b = seq_of_token(a.seqs, a.B, t);
-        const SeqDesc sd = a.seqs[b];
-        const int x = sd.kv_len - sd.q_len + (t - sd.q_start);
-        const int page = x / P, row = x - page * P;
-        const int32_t base = a.indptr[b];
-        if (page >= a.indptr[b + 1] - base) { atomicOr(a.err, 2); continue; }
-        const int32_t slot = a.indices[base + page];
-        if (slot < 0 || slot >= a.num_slots) { atomicOr(a.err, 2); continue; }
-        src[j] = ((int64_t)t * a.Hkv + g) * kHD + ch * 8;
-        dst[j] = (((int64_t)slot * a.Hkv + g) * P + row) * kHD + ch * 8;
+    for (int u = 0; u < kDepth; ++u) {
+      const int c = c0 + u * (int)blockDim.x;
+      dst[u] = -1;
+      if (c >= n) continue;
+      const int tok = tb + (c >> 4), ch = c & 15;
+      const int x = pre + tok;
+      const int page = x / P, row = x - page * P;
+      const int32_t slot = page < pt_count ? a.indices[pt_base + page] : -1;
+      if (slot < 0 || slot >= a.num_slots) {
+        atomicOr(a.err, 2);
+        continue;
       }
-      u32x4 kx[4], vx[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (src[j] >= 0) {
-          kx[j] = ld_u32x4(a.k_new + src[j]);
-          vx[j] = ld_u32x4(a.v_new + src[j]);
-        }
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (src[j] >= 0) {
-          st_u32x4(kp + dst[j], kx[j]);
-          st_u32x4(vp + dst[j], vx[j]);
-        }
+      const int64_t src = ((int64_t)(it.q_start + tok) * a.Hkv + it.kvh) * kHD + ch * 8;
+      kx[u] = ld_u32x4(a.k_new + src);
+      vx[u] = ld_u32x4(a.v_new + src);
+      dst[u] = (((int64_t)slot * a.Hkv + it.kvh) * P + row) * kHD + ch * 8;
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-    __hip_atomic_fetch_add(a.sync + kSyncStride, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-}
-
-// One wave: returns once every ticket is written (or the poll bound is hit).
-// Every lane polls, so no region of one lane sits in the caller's loop.
-__device__ __forceinline__ void app_wait(const AttnArgs& a) {
-  for (int n = 0;; ++n) {
-    const uint32_t done = __hip_atomic_load(a.sync + kSyncStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (done >= (uint32_t)a.app_tickets) break;
-    if (n == kAppSpinLimit) {
-      atomicOr(a.err, 8);
-      break;
-    }
-    __builtin_amdgcn_s_sleep(8);
-  }
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-}
-
-// Every thread of the block calls this once, at its end.
-__device__ __forceinline__ void app_finish(const AttnArgs& a) {
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const uint32_t n = __hip_atomic_fetch_add(a.sync + 2 * kSyncStride, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (n + 1 == gridDim.x)
 #pragma unroll
-      for (int k = 0; k < 3; ++k) __hip_atomic_store(a.sync + k * kSyncStride, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (int u = 0; u < kDepth; ++u)
+      if (dst[u] >= 0) {
+        st_u32x4(kp + dst[u], kx[u]);
+        st_u32x4(vp + dst[u], vx[u]);
+      }
   }
 }
 
@@ -212,10 +169,17 @@ __device__ __forceinline__ void app_finish(const AttnArgs& a) {
 // kPoolRsrc: a layer's K (and V) pool spans < 2^31 bytes, so one buffer
 // resource per pool reaches every page through the 32-bit scalar offset;
 // otherwise each page load builds a resource for its page.
-template <int P, bool kPoolRsrc, int kGroups, int GRP, bool kApp = false, bool kExact = false>
+//
+// kRead: keys from kv_len - q_len on (the segment's) are loaded from k_new /
+// v_new instead of from their pages (write_own_rows).  Within a tile the
+// source is chosen per group of four keys; a group holding keys of both kinds
+// (prefix lengths that are not a multiple of 4) takes the checked load, so the
+// steps that load its tile are plain steps.
+template <int P, bool kPoolRsrc, int kGroups, int GRP, bool kRead = false, bool kExact = false>
 __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs& a, const AttnItem& it,
                                                                  const SeqDesc& sd, const PipeLds& L) {
   static_assert(P == 16 || P == 32, "page size");
+  static_assert(!kRead || (kPoolRsrc && kGroups == 1), "segment reads: one group, pool-wide resources");
   constexpr int WAVES = kPipeWaves;
   constexpr int kRows = kPipeRows;
   constexpr int kPagesPerTile = kKT / P;
@@ -277,6 +241,7 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
 
   struct Slots {
     int32_t s[kPagesPerTile];
+    int32_t ts;              // the tile's first key
   };
   auto fetch = [&](int t) __attribute__((always_inline)) {
     Slots S;
@@ -285,6 +250,7 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
       const int pg = t * kPagesPerTile + j;
       S.s[j] = (pg >= 0 && pg < pt_count) ? ld_uniform(a.indices + pt_base + pg) : -1;
     }
+    S.ts = t * kKT;
     return S;
   };
   auto slot_ok = [&](int32_t s) __attribute__((always_inline)) { return s >= 0 && s < a.num_slots; };
@@ -300,17 +266,39 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
   const __amdgpu_buffer_rsrc_t rsrc_v =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.v), (short)0, (int)pool_bytes, 0x00020000);
 
+  // kRead: the segment's rows.  Key 4 gb + (lane >> 4) of the tile starting
+  // at key ts is token q_start + ts + 4 gb + (lane >> 4) - pre of k_new; a
+  // lane's offset within its group of four keys (the row within the group
+  // and the swizzled chunk, which depends only on key % 16 for K and key % 4
+  // for V, and key = 16 j + 4 wave + (lane >> 4)) is the same for every j,
+  // and the group's start goes in the scalar offset.
+  const __amdgpu_buffer_rsrc_t rsrc_nk =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.k_new), (short)0, kRead ? (int)a.new_bytes : 0,
+                                        0x00020000);
+  const __amdgpu_buffer_rsrc_t rsrc_nv =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.v_new), (short)0, kRead ? (int)a.new_bytes : 0,
+                                        0x00020000);
+  const int nk_off = (koff[0] & 255) + (lane >> 4) * a.Hkv * (kHD * 2);
+  const int nv_off = (voff[0] & 255) + (lane >> 4) * a.Hkv * (kHD * 2);
+  auto new_soff = [&](int ts, int gb) __attribute__((always_inline)) {
+    return ((uint32_t)(sd.q_start + ts + 4 * gb - pre) * (uint32_t)a.Hkv + (uint32_t)it.kvh) * (uint32_t)(kHD * 2);
+  };
+  // the tile holding a group of four keys of both kinds, or -1
+  const int t_mixed = (kRead && (pre & 3) != 0) ? pre / kKT : -1;
+
   // global -> LDS loads of one operand (K or V) of tile t into dst
   auto load_op = [&](int t, const Slots& S, const char* base, const __amdgpu_buffer_rsrc_t& rsrc, const int* off,
-                     lds_u8* dst) __attribute__((always_inline)) {
+                     const __amdgpu_buffer_rsrc_t& nrsrc, int noff, lds_u8* dst) __attribute__((always_inline)) {
     const int ts = t * kKT;
-    if (table_ok && ts + kKT <= g_hi) {
+    if (table_ok && ts + kKT <= g_hi && t != t_mixed) {
 #pragma unroll
       for (int j = 0; j < kNJ; ++j) {
         const int gb = j * WAVES + wave;
         const int32_t slot = S.s[(4 * gb) / P];
         __attribute__((address_space(3))) void* d = (__attribute__((address_space(3))) void*)(dst + gb * 1024);
-        if constexpr (kPoolRsrc)
+        if (kRead && ts + 4 * gb >= pre)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(nrsrc, d, 16, noff, new_soff(ts, gb), 0, 0);
+        else if constexpr (kPoolRsrc)
           __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, d, 16, off[j], (uint32_t)slot * (uint32_t)slot_bytes, 0, 0);
         else
           lds_dma16(base + (int64_t)slot * slot_bytes, (uint32_t)slot_bytes, off[j], d);
@@ -321,13 +309,20 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
       for (int j = 0; j < kNJ; ++j) {
         const int gb = j * WAVES + wave;
         const int32_t s = S.s[(4 * gb) / P];
-        const bool page_needed = ts + 4 * gb < g_hi;
+        const int key = ts + 4 * gb + (lane >> 4);
+        // the group's page is read when it holds keys of the item taken from pages
+        const bool page_needed = ts + 4 * gb < g_hi && (!kRead || ts + 4 * gb < pre);
         bad |= page_needed && !slot_ok(s);
-        const bool ld = page_needed && slot_ok(s) && ts + 4 * gb + (lane >> 4) < g_hi;
-        if (ld) {
-          lds_dma16(base + (int64_t)s * slot_bytes, (uint32_t)slot_bytes, off[j],
-                    (__attribute__((address_space(3))) void*)(dst + gb * 1024));
-        } else {
+        const bool ld = page_needed && slot_ok(s) && key < g_hi && (!kRead || key < pre);
+        const bool ldn = kRead && key < g_hi && key >= pre;
+        __attribute__((address_space(3))) void* d = (__attribute__((address_space(3))) void*)(dst + gb * 1024);
+        if (ld) lds_dma16(base + (int64_t)s * slot_bytes, (uint32_t)slot_bytes, off[j], d);
+        if constexpr (kRead) {
+          if (ldn)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                nrsrc, d, 16, (off[j] & 255) + ((sd.q_start + key - pre) * a.Hkv + it.kvh) * (kHD * 2), 0, 0, 0);
+        }
+        if (!ld && !ldn) {
           // absent keys: zero rows keep the masked products finite
           const u32x4 z = {0u, 0u, 0u, 0u};
           *(__attribute__((address_space(3))) u32x4*)(dst + gb * 1024 + lane * 16) = z;
@@ -342,7 +337,9 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
   for (int dt = 0; dt < 4; ++dt) oacc[dt] = f32x16{};
   float m_used = -INFINITY;  // exponent offset in use (log2 domain)
   float msub = 0.f;          // m_used, or 0 while it is -inf
+  float m_seen = -INFINITY;  // (exact scale) c times the row's largest score so far
   float l = 0.f;             // this lane's share of the denominator
+  float corr = 0.f;          // (exact scale) bf16 roundings of its rows' largest probabilities
   f32x16 negm = f32x16{};    // -msub in every element: where each S accumulation starts
   f32x16 sc[2][2];           // [buffer][32-key block] scores of tiles t and t + 1
   bf16x8 pop[4];             // [16-key group] probabilities of tile t
@@ -409,14 +406,29 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
         if (key > lim) S[kt][e] = -INFINITY;
       }
   };
-  // rescale test, given the row max mx of a tile's x values (raw scores with
-  // exact scale): move the offset when c (row max) outgrows it -- by any
-  // amount with exact scale, by 2^kRescaleLog2 when folded -- rescale O and
-  // l, and shift the tile's x values to the new offset
+  // rescale test, given this lane's max mx of a tile's x values (raw scores
+  // with exact scale): move the offset when c (row max) outgrows it by
+  // 2^kRescaleLog2, rescale O and l, and shift the tile's x values to the new
+  // offset.
+  // With exact scale the offset lags the row's max, so the largest
+  // probability of a row is 2^x for some x in [0, kRescaleLog2], which the
+  // bf16 packing of P rounds; the numerator then carries that rounding and
+  // the fp32 denominator would not.  Whenever a row's max grows, the lane
+  // holding the new largest score therefore adds its key's rounding,
+  // bf16(p) - p, to corr (rescaled with l): p is formed exactly as the tile's
+  // exponentials will form it (same fma, same offset), so the output, divided
+  // by l + corr, carries in numerator and denominator the same value for
+  // every key that was its row's largest when it arrived, as when the offset
+  // tracks every growth of the max (largest probability exactly 1), without
+  // the rescale of O that this would take at each growth.  The log-sum-exp
+  // takes l alone, the fp32 sum.
   auto rescale_test = [&](float mx, f32x16* X) __attribute__((always_inline)) {
+    const float mine = mx;
     mx = pair_max(mx);
     const float cand = kExact ? mx * a.c : mx + msub;       // c * row max
-    if (__ballot(cand > m_used + (kExact ? kRescaleLog2Exact : kRescaleLog2))) {
+    bool grew = false;
+    if constexpr (kExact) grew = __ballot(cand > m_seen) != 0;
+    if ((!kExact || grew) && __ballot(cand > m_used + kRescaleLog2)) {
       const float m_new = fmaxf(m_used, cand);
       const float alpha = (m_new == -INFINITY) ? 1.f : exp2f_fast(m_used - m_new);
       m_used = m_new;
@@ -430,6 +442,7 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
         for (int e = 0; e < 16; ++e) negm[e] = -msub;
       }
       l *= alpha;
+      if constexpr (kExact) corr *= alpha;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -443,6 +456,14 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
       } else {
         (void)shift;
         (void)X;
+      }
+    }
+    if constexpr (kExact) {
+      if (grew) {
+        const float p = exp2f_fast(__builtin_fmaf(mx, a.c, -msub));
+        const float d = (float)(__bf16)p - p;
+        corr += (cand > m_seen && mine == mx) ? d : 0.f;
+        m_seen = fmaxf(m_seen, cand);
       }
     }
   };
@@ -501,31 +522,41 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
   // interleaved step (next tile exists and needs no mask)
   Slots s_a, s_b;          // pages of tiles t + 1 and t + 2 in step t
 
-  // one 16-byte-per-lane page load of a full tile with an intact table
+  // one 16-byte-per-lane load of a full tile with an intact table: from the
+  // group's page, or (kRead) from the segment's rows, chosen without a branch
   auto tile_load = [&](const Slots& S, const char* base, const __amdgpu_buffer_rsrc_t& rsrc, const int* off,
-                       lds_u8* dst, int j) __attribute__((always_inline)) {
+                       const __amdgpu_buffer_rsrc_t& nrsrc, int noff, lds_u8* dst, int j) __attribute__((always_inline)) {
     const int gb = j * WAVES + wave;
     const int32_t slot = S.s[(4 * gb) / P];
     __attribute__((address_space(3))) void* d = (__attribute__((address_space(3))) void*)(dst + gb * 1024);
-    if constexpr (kPoolRsrc)
+    if constexpr (kRead) {
+      const bool seg = S.ts + 4 * gb >= pre;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(seg ? nrsrc : rsrc, d, 16, seg ? noff : off[j],
+                                               seg ? new_soff(S.ts, gb) : (uint32_t)slot * (uint32_t)slot_bytes, 0, 0);
+    } else if constexpr (kPoolRsrc) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, d, 16, off[j], (uint32_t)slot * (uint32_t)slot_bytes, 0, 0);
-    else
+    } else {
       lds_dma16(base + (int64_t)slot * slot_bytes, (uint32_t)slot_bytes, off[j], d);
+    }
   };
 
   // interleaved step; also issues this step's loads, K(t+2) into kn and
   // V(t+1) into vn (full tiles, intact table), one per MFMA of phase 1.
   // The exponentials of P(t) are split between the phases: the first
   // 4 kG1 pairs (16-key groups 0 .. kG1 - 1) between the S(t+1) MFMAs of
-  // phase 1, the rest between the first PV MFMAs of phase 2, each group
-  // finished before the PV MFMA that reads it.  Every VALU op waits on one
+  // phase 1, the rest between the PV MFMAs of phase 2, each group finished
+  // at least one MFMA before the PV MFMA that reads it.  Every VALU op waits on one
   // issued a step earlier, never on its neighbour, so the next MFMA issues on
   // time.
   auto fast_step = [&](auto bc, const lds_u8* kb, const lds_u8* vb, lds_u8* kn, lds_u8* vn) __attribute__((always_inline)) {
     constexpr int B = decltype(bc)::value, N = 1 - B;
     constexpr int E1 = 8 * kG1;              // exponentials in phase 1 (of 32)
     constexpr int E2 = 32 - E1;              // in phase 2
-    constexpr int W2 = kG1 < 4 ? 4 * kG1 : 1;    // phase-2 steps that take them
+    // phase-2 steps that take them: spread up to the step before the PV MFMA
+    // of the last group (slot 4 kG1 + 4 ... 12 with two groups per phase) needs
+    // it, rather than packed into the first 4 kG1 slots (measured ~1% faster at
+    // c2 with kG1 = 2)
+    constexpr int W2 = kG1 == 2 ? 11 : (kG1 < 4 ? 4 * kG1 : 1);
     // step of element e (pair e / 2, half e % 2); -1: before the first MFMA
     auto p1_step = [](int e) constexpr { return (e * 16) / E1 - 1; };
     auto p2_step = [](int e) constexpr { return ((e - E1) * W2) / (E2 > 0 ? E2 : 1) - 1; };
@@ -534,10 +565,22 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
     auto p2_pack = [&](int j) constexpr { return p2_step(2 * j + 1) + 1; };
     // row max of x(t+1), 16 three-way maxes: in the phase-2 steps past the exponentials
     auto mx_step = [](int k) constexpr { return kG1 <= 2 ? 8 + k / 2 : k; };
+    static_assert(phase2_in_time(kG1, W2), "a 16-key group of P packed after the PV MFMA that reads it");
     bf16x8 kop[16], vop[16];
     float ex[16][2];
-    float ls[2] = {0.f, 0.f};   // two accumulation chains for the denominator
-    auto do_exp = [&](int e) __attribute__((always_inline)) { ex[e >> 1][e & 1] = xexp(xpair(sc[B], e >> 1, e & 1)); };
+    // two accumulation chains for the denominator; -0 + y is y, so the first
+    // add of each chain folds away
+    float ls[2] = {-0.f, -0.f};
+    // (exact scale) exponents c s - m, each made one MFMA slot before its
+    // exponential, so the exponential never waits on the fma beside it
+    float xv[32];
+    auto do_x = [&](int e) __attribute__((always_inline)) {
+      if constexpr (kExact) xv[e] = __builtin_fmaf(xpair(sc[B], e >> 1, e & 1), a.c, -msub);
+    };
+    auto do_exp = [&](int e) __attribute__((always_inline)) {
+      if constexpr (kExact) ex[e >> 1][e & 1] = exp2f_fast(xv[e]);
+      else ex[e >> 1][e & 1] = exp2f_fast(xpair(sc[B], e >> 1, e & 1));
+    };
     auto do_pack = [&](int j) __attribute__((always_inline)) {
       ls[j & 1] += ex[j][0] + ex[j][1];
       pop[j >> 2][2 * (j & 3)] = (__bf16)ex[j][0];
@@ -548,17 +591,29 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
     for (int i = 0; i < kAhead; ++i) kop[i] = read_k(kb, i);
 #pragma unroll
     for (int e = 0; e < E1; ++e)
+      if (p1_step(e) <= 0) do_x(e);
+#pragma unroll
+    for (int e = 0; e < E1; ++e)
       if (p1_step(e) < 0) do_exp(e);
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       if (i + kAhead < 16) kop[i + kAhead] = read_k(kb, i + kAhead);
-      if (i < kNJ) tile_load(s_b, kbase, rsrc_k, koff, kn, i);
-      else if (i < 2 * kNJ) tile_load(s_a, vbase, rsrc_v, voff, vn, i - kNJ);
+      if (i < kNJ) tile_load(s_b, kbase, rsrc_k, koff, rsrc_nk, nk_off, kn, i);
+      else if (i < 2 * kNJ) tile_load(s_a, vbase, rsrc_v, voff, rsrc_nv, nv_off, vn, i - kNJ);
       s_step(sc[N], kop[i], i);
       int nv = 0;
 #pragma unroll
       for (int e = 0; e < E1; ++e)
         if (p1_step(e) == i) { do_exp(e); ++nv; }
+      if constexpr (kExact) {
+#pragma unroll
+        for (int e = 0; e < E1; ++e)
+          if (p1_step(e) == i + 1) { do_x(e); ++nv; }
+        // the exponents of the first elements of phase 2
+#pragma unroll
+        for (int e = E1; e < 32; ++e)
+          if (i == 15 && p2_step(e) < 0) { do_x(e); ++nv; }
+      }
 #pragma unroll
       for (int j = 0; j < E1 / 2; ++j)
         if (p1_pack(j) == i) { do_pack(j); nv += 3; }
@@ -581,6 +636,9 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
 #pragma unroll
     for (int e = E1; e < 32; ++e)
       if (p2_step(e) < 0) do_exp(e);
+#pragma unroll
+    for (int e = E1; e < 32; ++e)
+      if (p2_step(e) == 0) do_x(e);
     float mx[2] = {-INFINITY, -INFINITY};   // two accumulation chains
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
@@ -590,13 +648,18 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
 #pragma unroll
       for (int e = E1; e < 32; ++e)
         if (p2_step(e) == i) { do_exp(e); ++nv; }
+      if constexpr (kExact) {
+#pragma unroll
+        for (int e = E1; e < 32; ++e)
+          if (p2_step(e) == i + 1) { do_x(e); ++nv; }
+      }
 #pragma unroll
       for (int j = E1 / 2; j < 16; ++j)
         if (p2_pack(j) == i) { do_pack(j); nv += 3; }
 #pragma unroll
       for (int k = 0; k < 16; ++k)
         if (mx_step(k) == i) {
-          mx[k & 1] = vmax(mx[k & 1], vmax(sc[N][k & 1][2 * (k >> 1)], sc[N][k & 1][2 * (k >> 1) + 1]));
+          mx[k & 1] = vmax(vmax(mx[k & 1], sc[N][k & 1][2 * (k >> 1)]), sc[N][k & 1][2 * (k >> 1) + 1]);
           ++nv;
         }
       if (i + kAhead < 16) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
@@ -614,27 +677,14 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
   lds_u8* const V0 = L.v0;
   lds_u8* const V1 = L.v1;
 
-  // Tiles from t_seg on hold keys this launch appends: the step that issues
-  // the first such load waits for the append (step t loads tiles t + 1 and
-  // t + 2; the prologue loads t0 and t0 + 1).
-  int t_wait = -1;
-  if constexpr (kApp) {
-    static_assert(kGroups == 1, "the append runs with one group per block");
-    const int t_seg = pre / kKT;
-    if (t_seg < t1) {
-      if (t_seg <= t0 + 1) app_wait(a);
-      else t_wait = t_seg - 2;
-    }
-  }
-
   // ---- prologue: K(t0), V(t0), K(t0 + 1); S(t0) and its rescale test
   if (t0 < t1) {
     const Slots s0 = fetch(t0);
-    load_op(t0, s0, kbase, rsrc_k, koff, K0);
-    load_op(t0, s0, vbase, rsrc_v, voff, V0);
+    load_op(t0, s0, kbase, rsrc_k, koff, rsrc_nk, nk_off, K0);
+    load_op(t0, s0, vbase, rsrc_v, voff, rsrc_nv, nv_off, V0);
   }
   s_b = fetch(t0 + 1);
-  if (t0 + 1 < t1) load_op(t0 + 1, s_b, kbase, rsrc_k, koff, K1);
+  if (t0 + 1 < t1) load_op(t0 + 1, s_b, kbase, rsrc_k, koff, rsrc_nk, nk_off, K1);
   // Interleaved steps take the page slots of their loads from a vector load
   // issued a step ahead: it is counted with the tile loads and has a whole
   // step to land, where a scalar load would be waited for at the next barrier.
@@ -678,8 +728,8 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
   if (t_boost > t0) __builtin_amdgcn_s_setprio(1);
   auto top = [&](int t, lds_u8* kn, lds_u8* vn) __attribute__((always_inline)) {
     wait_tiles();
-    if (t + 2 < t1) load_op(t + 2, s_b, kbase, rsrc_k, koff, kn);
-    if (t + 1 < t1) load_op(t + 1, s_a, vbase, rsrc_v, voff, vn);
+    if (t + 2 < t1) load_op(t + 2, s_b, kbase, rsrc_k, koff, rsrc_nk, nk_off, kn);
+    if (t + 1 < t1) load_op(t + 1, s_a, vbase, rsrc_v, voff, rsrc_nv, nv_off, vn);
   };
   auto advance = [&](int t) __attribute__((always_inline)) {
     s_a = s_b;
@@ -691,6 +741,7 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
     s_a = s_b;
 #pragma unroll
     for (int j = 0; j < kPagesPerTile; ++j) s_b.s[j] = (int32_t)__builtin_amdgcn_readfirstlane(v_next[j]);
+    s_b.ts = (t + 2) * kKT;
     v_next = fetch_vec(t + 3);
   };
   // Steps t < t_fast interleave: their next tile needs no mask, V(t+1) is a
@@ -699,22 +750,21 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
   // them masks them), all covered by an intact table.  Waves run different
   // numbers of each kind of step but the same number of steps, each with one
   // barrier and its share of the tile loads.
-  const int t_fast = (wave_active && table_ok) ? max(t0, min(w_full / kKT - 1, t1 - 2)) : t0;
+  int t_fast = (wave_active && table_ok) ? max(t0, min(w_full / kKT - 1, t1 - 2)) : t0;
+  // (kRead) no interleaved step loads the tile with a mixed group of keys
+  if (t_mixed >= 0) t_fast = max(t0, min(t_fast, t_mixed - 2));
   int t = t0;
   for (; t + 1 < t_fast; t += 2) {
-    if (kApp && t == t_wait) app_wait(a);
     priority(t);
     wait_tiles();
     advance_fast(t);
     fast_step(IntC<0>{}, K1, V0, K0, V1);
-    if (kApp && t + 1 == t_wait) app_wait(a);
     priority(t + 1);
     wait_tiles();
     advance_fast(t + 1);
     fast_step(IntC<1>{}, K0, V1, K1, V0);
   }
   if (t < t_fast) {
-    if (kApp && t == t_wait) app_wait(a);
     priority(t);
     wait_tiles();
     advance_fast(t);
@@ -730,13 +780,17 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
   }
   for (; t < t1; ++t) {
     const bool odd = (t - t0) & 1;
-    if (kApp && t == t_wait) app_wait(a);
     priority(t);
     top(t, odd ? K1 : K0, odd ? V0 : V1);
     plain_step(t, odd ? K0 : K1, odd ? V1 : V0);
     advance(t);
   }
 
+  // (two groups) the partial results merge through l alone
+  if constexpr (kExact && kGroups == 2) {
+    l += corr;
+    corr = 0.f;
+  }
   if constexpr (kGroups == 2) {
     // Both groups pass the same number of barriers: group g has passed
     // 1 + g + 2 (its steps) so far; pad to the larger count, then one more
@@ -786,7 +840,8 @@ __device__ __attribute__((always_inline)) inline void pipe_group(const AttnArgs&
 
   if (!wave_active) return;
   const float l_tot = pair_sum(l);
-  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  const float l_out = kExact ? pair_sum(l + corr) : l_tot;
+  const float inv = l_out > 0.f ? 1.f / l_out : 0.f;
   const float lse2 = l_tot > 0.f ? m_used + __builtin_amdgcn_logf(l_tot) : -INFINITY;
   // The output row is worked out again from the lane index here rather than
   // kept from the start: values live across the loops beyond its registers
@@ -1131,14 +1186,18 @@ __device__ __attribute__((always_inline)) inline void decode_group(const AttnArg
 }
 
 // One group of four waves per block, two blocks per CU.
-// kApp: the launch also writes the segment's new K/V rows (app_produce).
+// kRead: the launch also writes the segment's new K/V rows (write_own_rows)
+// and reads the segment's keys from them, not from their pages.  A decode item
+// reads its keys through the pages: it is then the only reader of its rows, so
+// it writes them itself first and reads them back after a barrier; a later
+// key-range part of a split decode item that holds segment keys takes the
+// general path, which reads them from k_new / v_new.
 // kExact: the softmax scale is applied in fp32 to each score instead of to
 // the query rows in bf16 (one fma per score; no rounding of c q).
-template <int P, bool kPoolRsrc, bool kApp, bool kExact = false>
+template <int P, bool kPoolRsrc, bool kRead, bool kExact = false>
 __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t k_lds0[kTileBytes], k_lds1[kTileBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t v_lds0[kTileBytes], v_lds1[kTileBytes];
-  if constexpr (kApp) app_produce<P>(a);
   const AttnItem it = ld_uniform(a.items + blockIdx.x);
   if (a.blk_clock != nullptr && threadIdx.x == 0) {
     uint64_t* r = a.blk_clock + 4 * (int64_t)blockIdx.x;
@@ -1150,12 +1209,19 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
     const SeqDesc sd{it.q_start, it.q_len, it.kv_len, 0};
     const PipeLds L{(lds_u8*)k_lds0, (lds_u8*)k_lds1, (lds_u8*)v_lds0, (lds_u8*)v_lds1,
                     nullptr, nullptr, nullptr, nullptr, nullptr};
-    if (!kApp && kPoolRsrc && it.q_len * a.G <= kDecRows)
+    const bool decode = kPoolRsrc && it.q_len * a.G <= kDecRows &&
+                        (!kRead || it.kv_begin == 0 || it.kv_end <= it.kv_len - it.q_len);
+    if constexpr (kRead) {
+      if (it.kv_begin == 0) {
+        write_own_rows<P>(a, it);
+        if (decode) __syncthreads();                         // its own rows, read back below
+      }
+    }
+    if (decode)
       decode_group<P, kExact>(a, it, sd, L);
     else
-      pipe_group<P, kPoolRsrc, 1, 0, kApp, kExact>(a, it, sd, L);
+      pipe_group<P, kPoolRsrc, 1, 0, kRead, kExact>(a, it, sd, L);
   }
-  if constexpr (kApp) app_finish(a);
   if (a.blk_clock != nullptr) {
     // every wave's stores are done once the barrier is passed
     __syncthreads();

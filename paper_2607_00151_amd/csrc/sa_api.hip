@@ -119,8 +119,8 @@ struct sa_ctx {
   int ring_next = 0;
   float* part = nullptr;           // split-KV partials
   size_t part_cap = 0;             // bytes
-  uint32_t* d_sync = nullptr;      // counters of an attention launch that appends (zero between launches)
   bool exact_scale = true;         // sa_set_exact_scale (0: scale folded into q)
+  bool fused_append = false;       // sa_set_fused_append (0, the default: append launch, then attention)
   hipEvent_t kernel_ev[2][2] = {};   // sa_set_kernel_events: [SA_TIMED_ATTN | SA_TIMED_PAGES][start, stop]
   uint64_t* blk_clock = nullptr;     // sa_set_block_clock: device buffer, 4 words per block
   int64_t blk_clock_cap = 0;         // blocks it holds
@@ -261,19 +261,6 @@ AttnVariant attn_variant() {
   return kVariants[v];
 }
 
-// sa_segment_prefill_attn_append writes the segment's rows with the append
-// kernel and then runs the attention (two launches) unless
-// SA_APPEND_IN_ATTN=1, which has the default attention kernel write them
-// itself in the same launch (measured slower at the c2 workload: the
-// cross-block publication of the rows costs more than the launch it saves).
-bool append_in_attention() {
-  static bool v = [] {
-    const char* e = getenv("SA_APPEND_IN_ATTN");
-    return e != nullptr && atoi(e) == 1;
-  }();
-  return v;
-}
-
 // A kernel launch; with timing events set (sa_set_kernel_events) it goes
 // through hipExtLaunchKernelGGL, which binds both events to the kernel itself,
 // so their elapsed time is the kernel's execution on the device.
@@ -285,10 +272,16 @@ void launch_timed(K kernel, dim3 grid, dim3 block, hipStream_t st, const hipEven
     hipLaunchKernelGGL(kernel, grid, block, 0, st, a);
 }
 
+// read: the pipelined kernel that also writes the segment's rows and reads
+// the segment's keys from them (pool_rsrc only)
 template <int P>
-void launch_attn_p(AttnVariant v, bool pool_rsrc, bool exact, dim3 grid, hipStream_t st, const hipEvent_t* ev,
-                   const sa::AttnArgs& a) {
-  if (v.pipe == 1 && exact && pool_rsrc)
+void launch_attn_p(AttnVariant v, bool pool_rsrc, bool exact, bool read, dim3 grid, hipStream_t st,
+                   const hipEvent_t* ev, const sa::AttnArgs& a) {
+  if (v.pipe == 1 && read && exact)
+    launch_timed(sa::attn_pipe_kernel<P, true, true, true>, grid, dim3(256), st, ev, a);
+  else if (v.pipe == 1 && read)
+    launch_timed(sa::attn_pipe_kernel<P, true, true, false>, grid, dim3(256), st, ev, a);
+  else if (v.pipe == 1 && exact && pool_rsrc)
     launch_timed(sa::attn_pipe_kernel<P, true, false, true>, grid, dim3(256), st, ev, a);
   else if (v.pipe == 1 && exact)
     launch_timed(sa::attn_pipe_kernel<P, false, false, true>, grid, dim3(256), st, ev, a);
@@ -296,10 +289,6 @@ void launch_attn_p(AttnVariant v, bool pool_rsrc, bool exact, dim3 grid, hipStre
     launch_timed(sa::attn_pp_kernel<P, true>, grid, dim3(512), st, ev, a);
   else if (v.pipe == 2)
     launch_timed(sa::attn_pp_kernel<P, false>, grid, dim3(512), st, ev, a);
-  else if (v.pipe && a.app_tickets > 0 && pool_rsrc)
-    launch_timed(sa::attn_pipe_kernel<P, true, true>, grid, dim3(256), st, ev, a);
-  else if (v.pipe && a.app_tickets > 0)
-    launch_timed(sa::attn_pipe_kernel<P, false, true>, grid, dim3(256), st, ev, a);
   else if (v.pipe && pool_rsrc)
     launch_timed(sa::attn_pipe_kernel<P, true, false>, grid, dim3(256), st, ev, a);
   else if (v.pipe)
@@ -310,10 +299,10 @@ void launch_attn_p(AttnVariant v, bool pool_rsrc, bool exact, dim3 grid, hipStre
 
 // pool_rsrc: a layer's K (and V) pool spans < 2^31 bytes, so one buffer
 // resource per pool addresses every page with a 32-bit offset
-void launch_attn(int page_size, AttnVariant v, bool pool_rsrc, bool exact, dim3 grid, hipStream_t st,
+void launch_attn(int page_size, AttnVariant v, bool pool_rsrc, bool exact, bool read, dim3 grid, hipStream_t st,
                  const hipEvent_t* ev, const sa::AttnArgs& a) {
-  if (page_size == 16) launch_attn_p<16>(v, pool_rsrc, exact, grid, st, ev, a);
-  else launch_attn_p<32>(v, pool_rsrc, exact, grid, st, ev, a);
+  if (page_size == 16) launch_attn_p<16>(v, pool_rsrc, exact, read, grid, st, ev, a);
+  else launch_attn_p<32>(v, pool_rsrc, exact, read, grid, st, ev, a);
 }
 
 }  // namespace
@@ -354,9 +343,6 @@ sa_status sa_create(int device, sa_ctx** out) {
   c->num_cu = prop.multiProcessorCount;
   hipError_t e = hipMalloc(&c->d_err, sizeof(int32_t));
   if (e == hipSuccess) e = hipMemset(c->d_err, 0, sizeof(int32_t));
-  const size_t sync_bytes = 3 * sa::kSyncStride * sizeof(uint32_t);
-  if (e == hipSuccess) e = hipMalloc(&c->d_sync, sync_bytes);
-  if (e == hipSuccess) e = hipMemset(c->d_sync, 0, sync_bytes);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   for (int i = 0; e == hipSuccess && i < kRing; ++i)
     e = hipEventCreateWithFlags(&c->ring[i].ev, hipEventDisableTiming);
@@ -384,7 +370,6 @@ void sa_destroy(sa_ctx* ctx) {
   if (ctx->part) (void)hipFree(ctx->part);
   for (void* p : ctx->retired_dev) (void)hipFree(p);
   for (void* p : ctx->retired_host) (void)hipHostFree(p);
-  if (ctx->d_sync) (void)hipFree(ctx->d_sync);
   if (ctx->d_err) (void)hipFree(ctx->d_err);
   if (ctx->na_host) (void)hipHostFree(ctx->na_host);
   if (ctx->na_ev) (void)hipEventDestroy(ctx->na_ev);
@@ -691,10 +676,11 @@ sa_status sa_kv_splice_alias(sa_ctx* ctx, const sa_layout* layout, int32_t batch
 
 namespace {
 
-// The attention launch; with `append` it first writes each sequence's q_len
-// new K/V rows (k_new, v_new) to its positions kv_len - q_len .. kv_len - 1:
-// as an append launch before the attention, or inside the attention launch
-// (append_in_attention()).
+// The attention launch; with `append` each sequence's q_len new K/V rows
+// (k_new, v_new) also go to its positions kv_len - q_len .. kv_len - 1: by the
+// attention launch itself, which then reads the segment's keys from k_new /
+// v_new (ctx->fused_append, the pipelined kernel, a pool and new rows that a
+// buffer resource spans), else by an append launch before the attention.
 //
 // With `noalloc` the plan and the split partials go to this device's fixed
 // `scratch` array (no append then): the plan must fit kNoAllocPlanBytes, and
@@ -724,9 +710,21 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
 
   // ---- kernel variant: query rows per wave (32 * qt) and waves per work item
   const AttnVariant var = attn_variant();
-  // the exact-scale form of the pipelined kernel has no in-launch append
   const bool exact = ctx->exact_scale && var.pipe == 1;
-  const bool fused = append && var.pipe == 1 && !exact && append_in_attention();
+  const bool pool_rsrc = layer_elems(layout) * 2 < ((int64_t)1 << 31);
+  const int64_t new_bytes = total_q * Hkv * sa::kHD * 2;
+  const bool fused = append && ctx->fused_append && var.pipe == 1 && pool_rsrc && new_bytes < ((int64_t)1 << 31);
+  if (fused && debug_checks()) {
+    // the rows the launch writes (sa_kv_append checks its own): no two
+    // sequences write one slot row
+    std::vector<int32_t> ip, ix, start(batch);
+    s = fetch_table(pages.indptr, pages.indices, batch, (hipStream_t)stream, ip, ix);
+    if (s != SA_OK) return s;
+    for (int b = 0; b < batch; ++b) start[b] = h_kv_len[b] - h_q_len[b];
+    s = sa::debug_check_append(batch, start.data(), h_q_len, ip.data(), ix.data(), layout->page_size,
+                               layout->num_slots, g_err);
+    if (s != SA_OK) return s;
+  }
   if (append && !fused) {
     // the new rows go in with an append launch of their own
     std::vector<int32_t> start(batch);
@@ -809,16 +807,10 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
   a.Hkv = Hkv;
   a.G = G;
   a.c = softmax_scale * 1.4426950408889634f;
-  a.B = batch;
   if (fused) {
     a.k_new = (const uint16_t*)k_new;
     a.v_new = (const uint16_t*)v_new;
-    a.sync = ctx->d_sync;
-    a.app_chunks = total_q * Hkv * 16;
-    // whole groups of 64 tickets (one wave's draw) cover the chunks
-    const int64_t tickets = (a.app_chunks + 64 * sa::kAppTicket - 1) / (64 * sa::kAppTicket) * 64;
-    if (tickets > INT32_MAX / 2) return fail(SA_ERR_SHAPE, "too many new rows for one launch");
-    a.app_tickets = (int32_t)tickets;
+    a.new_bytes = (uint32_t)new_bytes;
   }
   if (ctx->blk_clock != nullptr && var.pipe == 1) {
     if ((int64_t)items.size() > ctx->blk_clock_cap)
@@ -826,8 +818,7 @@ sa_status attn_launch(sa_ctx* ctx, const sa_layout* layout, int32_t layer, const
                   (long long)ctx->blk_clock_cap, items.size());
     a.blk_clock = ctx->blk_clock;
   }
-  const bool pool_rsrc = layer_elems(layout) * 2 < ((int64_t)1 << 31);
-  launch_attn(layout->page_size, var, pool_rsrc, exact, dim3((unsigned)items.size()), (hipStream_t)stream,
+  launch_attn(layout->page_size, var, pool_rsrc, exact, fused, dim3((unsigned)items.size()), (hipStream_t)stream,
               ctx->kernel_ev[SA_TIMED_ATTN], a);
   SA_HIP(hipGetLastError());
   if (!groups.empty()) {
@@ -897,6 +888,13 @@ sa_status sa_set_exact_scale(sa_ctx* ctx, int32_t enable) {
   sa_status s = check_ctx(ctx);
   if (s != SA_OK) return s;
   ctx->exact_scale = enable != 0;
+  return SA_OK;
+}
+
+sa_status sa_set_fused_append(sa_ctx* ctx, int32_t enable) {
+  sa_status s = check_ctx(ctx);
+  if (s != SA_OK) return s;
+  ctx->fused_append = enable != 0;
   return SA_OK;
 }
 
