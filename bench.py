@@ -158,7 +158,7 @@ def calibrate_xcds(ctx, run, launches: int = 5, settle: int = 20, refine: int = 
         run(i)
         torch.cuda.synchronize()
         r = cbuf.view(-1, 4).cpu().numpy()
-        ids = np.nonzero((r[:, 0] != -1) & (r[:, 3] != 0))[0]
+        ids = np.nonzero((r[:, 0] != -1) & ((r[:, 3] & 0xffffffff) != 0))[0]
         acc += [float(np.mean(r[ids[ids % 8 == x], 1] - r[ids[ids % 8 == x], 0])) for x in range(8)]
     speed = acc.mean() / acc
     sa.sa_set_xcd_weights(ctx, speed)
@@ -173,7 +173,7 @@ def calibrate_xcds(ctx, run, launches: int = 5, settle: int = 20, refine: int = 
             n += 1
             torch.cuda.synchronize()
             r = cbuf.view(-1, 4).cpu().numpy()
-            ids = np.nonzero((r[:, 0] != -1) & (r[:, 3] != 0))[0]
+            ids = np.nonzero((r[:, 0] != -1) & ((r[:, 3] & 0xffffffff) != 0))[0]
             t0 = r[ids, 0].min()
             ends += [float(r[ids[ids % 8 == x], 1].max() - t0) for x in range(8)]
         speed = speed * (ends.mean() / ends)
@@ -447,12 +447,12 @@ def config_mode(args):
             sa.sa_segment_prefill_attn(ctx, L, 0, q, kp, vp, w.qlen, w.kv, pages[0], pages[1], w.scale, o, lse)
             torch.cuda.synchronize()
             r = buf.view(-1, 4).cpu().numpy()
-            r = r[(r[:, 0] != -1) & (r[:, 3] != 0)]
+            r = r[(r[:, 0] != -1) & ((r[:, 3] & 0xffffffff) != 0)]
             t0c = r[:, 0].min()
             to_ms = 1.0 / khz
             spans.append((r[:, 1].max() - t0c) * to_ms)
-            dec_done.append((r[r[:, 3] == 1, 1].max() - t0c) * to_ms)
-            pre_done.append((r[r[:, 3] > 1, 1].max() - t0c) * to_ms)
+            dec_done.append((r[(r[:, 3] & 0xffffffff) == 1, 1].max() - t0c) * to_ms)
+            pre_done.append((r[(r[:, 3] & 0xffffffff) > 1, 1].max() - t0c) * to_ms)
         sa.sa_set_block_clock(ctx, None)
         sa.sa_sync_check(ctx)
         rec["mixed_launch_clock"] = {

@@ -376,9 +376,12 @@ sa_status sa_set_kernel_events(sa_ctx *ctx, int32_t which, void *start_event, vo
  * decode requests with prefill chunks).  While set, each launch of the default
  * attention kernel writes, for every workgroup w, four uint64 words at
  * d_buf[4w]: the device's constant-rate wall clock (s_memrealtime) when w
- * started and when all its output stores were done, its sequence index and
- * that sequence's q_len (1: a decode row; 0 for a workgroup with no work, which
- * the planner adds to even out the XCDs).  The launch has one workgroup per
+ * started and when all its output stores were done; then its work item: word
+ * 2 holds the sequence index in bits 0-31, the KV head in bits 32-47 and the
+ * item's first key tile (of 64 keys) modulo 2^16 in bits 48-63; word 3 holds
+ * that sequence's q_len in bits 0-31 (1: a decode row; 0 for a workgroup with
+ * no work, which the planner adds to even out the XCDs) and the item's first
+ * packed query row in bits 32-63.  The launch has one workgroup per
  * work item, at most max_blocks of them, else it fails with SA_ERR_SHAPE
  * before launching.  d_buf: device memory of 32 * max_blocks bytes, 8-byte
  * aligned, owned by the caller; the words of one launch are overwritten by

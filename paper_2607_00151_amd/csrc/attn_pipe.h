@@ -1202,8 +1202,10 @@ __global__ __launch_bounds__(256, 2) void attn_pipe_kernel(AttnArgs a) {
   if (a.blk_clock != nullptr && threadIdx.x == 0) {
     uint64_t* r = a.blk_clock + 4 * (int64_t)blockIdx.x;
     r[0] = __builtin_amdgcn_s_memrealtime();
-    r[2] = (uint64_t)(uint32_t)it.seq;
-    r[3] = (uint64_t)(uint32_t)it.q_len;
+    // {sequence, KV head, first key tile mod 2^16}, {q_len, first row}
+    r[2] = (uint64_t)(uint32_t)it.seq | ((uint64_t)(uint16_t)it.kvh << 32) |
+           ((uint64_t)(uint16_t)(it.kv_begin / kKT) << 48);
+    r[3] = (uint64_t)(uint32_t)it.q_len | ((uint64_t)(uint32_t)it.row0 << 32);
   }
   if (it.kv_begin < it.kv_end) {                            // else a padding item
     const SeqDesc sd{it.q_start, it.q_len, it.kv_len, 0};

@@ -70,11 +70,16 @@ def small(name):
         return build(name, 11, 32, 2, 128, 16, [64, 3], [50, 9])
     if name == "g3_p16":
         return build(name, 12, 6, 2, 128, 16, [45, 0, 300], [43, 70, 2], assemble=True)
+    if name == "zero_len":
+        # sequences with no new tokens first, in the middle (one with no cache at all)
+        # and last, beside a decode row and segments over partial pages
+        return build(name, 13, 8, 2, 128, 16, [40, 300, 0, 64, 17, 5], [0, 90, 0, 130, 0, 1],
+                     assemble=True)
     raise KeyError(name)
 
 
-SMALL = ["c1", "ragged_g4_p16", "g8_p32_outliers", "g1_p16", "g2_p32", "g16_p16", "g3_p16"]
-WITH_ASM = ["ragged_g4_p16", "g8_p32_outliers", "g1_p16", "g3_p16"]
+SMALL = ["c1", "ragged_g4_p16", "g8_p32_outliers", "g1_p16", "g2_p32", "g16_p16", "g3_p16", "zero_len"]
+WITH_ASM = ["ragged_g4_p16", "g8_p32_outliers", "g1_p16", "g3_p16", "zero_len"]
 
 
 def oracle_all(w):
@@ -722,9 +727,13 @@ def test_block_clock_records(ctx):
     assert n > 0 and (rec[n:] == -1).all()          # one record per workgroup, nothing beyond
     rec = rec[:n]
     assert (rec[:, 1] >= rec[:, 0]).all()
-    rec = rec[rec[:, 3] != 0]                        # workgroups of padding items report q_len 0
-    assert set(rec[:, 2].tolist()) == set(range(w.batch))
-    assert np.array_equal(rec[:, 3], w.qlen[rec[:, 2]])
+    it = clock_items(rec)
+    live = it["q_len"] != 0                          # workgroups of padding items report q_len 0
+    assert set(it["seq"][live].tolist()) == set(range(w.batch))
+    assert np.array_equal(it["q_len"][live], w.qlen[it["seq"][live]])
+    assert (it["kvh"][live] < w.num_kv_heads).all()
+    G = w.num_q_heads // w.num_kv_heads
+    assert (it["row0"][live] % 32 == 0).all() and (it["row0"][live] < w.qlen[it["seq"][live]] * G).all()
     span_us = (rec[:, 1].max() - rec[:, 0].min()) / khz * 1e3
     print(f"  {n} workgroups, clock {khz} kHz, span {span_us:.1f} us", flush=True)
     # a buffer too small for the launch is refused before anything runs
@@ -735,6 +744,81 @@ def test_block_clock_records(ctx):
             attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
     finally:
         sa.sa_set_block_clock(ctx, None)
+
+
+def clock_items(rec):
+    """The work item of each sa_set_block_clock record: sequence, KV head, first key
+    tile (mod 2^16), q_len and first packed query row."""
+    w2, w3 = rec[:, 2], rec[:, 3]
+    return {"seq": w2 & 0xFFFFFFFF, "kvh": (w2 >> 32) & 0xFFFF, "tile": (w2 >> 48) & 0xFFFF,
+            "q_len": w3 & 0xFFFFFFFF, "row0": (w3 >> 32) & 0xFFFFFFFF}
+
+
+def test_xcd_weights_two_rounds_every_item_once(ctx):
+    """A launch of 512 work items (two per CU: the planner's swap search between XCDs),
+    weighted twice in a row (the second call reuses the first's weighting): output and LSE
+    equal the unweighted launch's bit for bit; every launch runs each (sequence, KV head,
+    row tile, key tile) item exactly once; the second weighted launch places the items as
+    the first did; and the XCD given 0.8 of the others' speed gets fewer key tiles."""
+    w = build("xcdw2", 33, 32, 8, 128, 16, [3000], [2048])
+    print("xcd weights, two rounds: Hq 32 / Hkv 8, pre 3000, q 2048", flush=True)
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    buf = torch.full((4 * 4096,), -1, dtype=torch.int64, device="cuda")
+    G = w.num_q_heads // w.num_kv_heads
+    pre, kv = int(w.pre[0]), int(w.kv[0])
+
+    def run():
+        buf.fill_(-1)
+        sa.sa_set_block_clock(ctx, buf)
+        try:
+            o, lse = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+        finally:
+            sa.sa_set_block_clock(ctx, None)
+        torch.cuda.synchronize()
+        rec = buf.view(-1, 4).cpu().numpy().copy()
+        n = int((rec[:, 0] != -1).sum())
+        return o, lse, clock_items(rec[:n])
+
+    def items(it):
+        live = np.nonzero(it["q_len"] != 0)[0]
+        keys = [(int(it["seq"][i]), int(it["kvh"][i]), int(it["row0"][i]), int(it["tile"][i])) for i in live]
+        assert len(keys) == len(set(keys))                         # no item twice
+        return keys, live
+
+    def xcd_tiles(it, x):
+        keys, live = items(it)
+        tiles = 0
+        for (s_, h, r0, t0), i in zip(keys, live):
+            if i % 8 != x:
+                continue
+            end = min(kv, pre + (r0 + 128 + G - 1) // G)           # the row tile's last visible key + 1
+            tiles += (end + 63) // 64 - t0
+        return tiles
+
+    o1, lse1, r1 = run()
+    sa.sa_set_xcd_weights(ctx, [1, 1, 1, 1, 1, 1, 1, 0.8])
+    try:
+        o2, lse2, r2 = run()
+        o3, lse3, r3 = run()
+    finally:
+        sa.sa_set_xcd_weights(ctx, None)
+    sa.sa_sync_check(ctx)
+    for o_, l_ in ((o2, lse2), (o3, lse3)):
+        assert torch.equal(o1, o_) and torch.equal(lse1, l_)
+    k1, _ = items(r1)
+    k2, l2 = items(r2)
+    k3, l3 = items(r3)
+    assert len(k1) == 512 and set(k1) == set(k2) == set(k3)
+    assert [(int(i), k) for i, k in zip(l2, k2)] == [(int(i), k) for i, k in zip(l3, k3)]
+    t_before, t_after = xcd_tiles(r1, 7), xcd_tiles(r2, 7)
+    others = [xcd_tiles(r2, x) for x in range(7)]
+    print(f"  XCD 7 key tiles {t_before} -> {t_after}; others {min(others)}..{max(others)}", flush=True)
+    assert t_after < t_before and t_after < min(others)
+    toks, heads = sample_rows(w, 64)
+    ref, ref_lse, _ = oracle.attention_rows(w.q, w.k, w.v, w.q_indptr, w.kv_indptr,
+                                            w.num_q_heads, w.num_kv_heads, w.scale, toks, heads)
+    compare(host_u16(o2)[toks, heads], ref, MAX_TOL, MEAN_TOL)
 
 
 def test_xcd_weights_move_work_not_results(ctx):
