@@ -292,12 +292,17 @@ inline int64_t busiest_cu(const std::vector<AttnItem>& q, size_t round) {
 // The XCDs of one chip do not run equally fast under this load (measured:
 // the slowest one's workgroups take ~5-7% longer than the fastest one's on
 // the same work, whichever KV head it serves), and the launch ends with the
-// slowest.  Given relative speeds, move work from the XCD whose busiest CU
-// has the most key tiles per unit of speed to the one with the fewest, by
-// swapping the longest item of the first for the shortest of the second
-// while neither ends above the first's present cost: every XCD keeps its
-// number of items, so the launch keeps its rounds; the items that move read
-// another KV head's K/V than their XCD's others, which the balance pays for.
+// slowest.  Given relative speeds, the XCDs are paired by speed -- the
+// slowest with the fastest, the second slowest with the second fastest, and
+// so on -- and within each pair work moves from the one whose busiest CU has
+// the more key tiles per unit of speed to the other, by swapping the longest
+// item of the first for the shortest of the second while neither ends above
+// the first's present cost.  Every XCD keeps its number of items, so the
+// launch keeps its rounds.  An item that moves reads another KV head's K/V
+// than its XCD's others, through that XCD's L2: keeping the exchanges inside
+// fixed pairs bounds those foreign KV heads at one per XCD (measured at c2:
+// a search over all XCDs reached 20-28 foreign (KV head, XCD) pairs and 2.6x
+// the HBM reads of the unweighted launch for ~0.5% more balance).
 // Queues of at most two rounds come back sorted longest first.
 inline void weigh_xcds(std::vector<std::vector<AttnItem>>& queue, size_t round, const float* speed) {
   // More than two rounds: each XCD's CUs take its items as they free; moving
@@ -307,31 +312,33 @@ inline void weigh_xcds(std::vector<std::vector<AttnItem>>& queue, size_t round, 
   for (const auto& q : queue)
     if (q.size() > 2 * round) return;
   for (auto& q : queue) sort_longest_first(q);
-  double cost[kNumXcd];
-  for (int x = 0; x < kNumXcd; ++x) cost[x] = busiest_cu(queue[x], round) / speed[x];
-  for (int iter = 0; iter < 4096; ++iter) {
-    int s = 0, f = 0;
-    for (int x = 1; x < kNumXcd; ++x) {
-      if (cost[x] > cost[s]) s = x;
-      if (cost[x] < cost[f]) f = x;
+  int order[kNumXcd];
+  for (int x = 0; x < kNumXcd; ++x) order[x] = x;
+  std::stable_sort(order, order + kNumXcd, [&](int a, int b) { return speed[a] < speed[b]; });
+  for (int k = 0; k < kNumXcd / 2; ++k) {
+    const int x0 = order[k], x1 = order[kNumXcd - 1 - k];
+    double c0 = busiest_cu(queue[x0], round) / speed[x0], c1 = busiest_cu(queue[x1], round) / speed[x1];
+    for (int iter = 0; iter < 4096 && c0 != c1; ++iter) {
+      const bool first = c0 > c1;               // the more loaded of the pair gives
+      const int s = first ? x0 : x1, f = first ? x1 : x0;
+      const double cs = first ? c0 : c1;
+      auto& qs = queue[s];
+      auto& qf = queue[f];
+      if (qs.empty() || qf.empty() || item_tiles(qs.front()) <= item_tiles(qf.back())) break;
+      std::vector<AttnItem> ns = qs, nf = qf;
+      std::swap(ns.front(), nf.back());
+      sort_longest_first(ns);
+      sort_longest_first(nf);
+      // a swap may leave s's busiest CU where it was (another CU of s carries as
+      // much): it is taken as long as neither XCD ends above s's present cost,
+      // since it lowers s's total and the next swaps then lower that CU
+      const double ns_c = busiest_cu(ns, round) / speed[s], nf_c = busiest_cu(nf, round) / speed[f];
+      if (ns_c > cs || nf_c >= cs) break;
+      qs.swap(ns);
+      qf.swap(nf);
+      (first ? c0 : c1) = ns_c;
+      (first ? c1 : c0) = nf_c;
     }
-    if (s == f || queue[s].empty() || queue[f].empty()) return;
-    auto& qs = queue[s];
-    auto& qf = queue[f];
-    if (item_tiles(qs.front()) <= item_tiles(qf.back())) return;
-    std::vector<AttnItem> ns = qs, nf = qf;
-    std::swap(ns.front(), nf.back());
-    sort_longest_first(ns);
-    sort_longest_first(nf);
-    // a swap may leave s's busiest CU where it was (another CU of s carries as
-    // much): it is taken as long as neither XCD ends above s's present cost,
-    // since it lowers s's total and the next swaps then lower that CU
-    const double cs = busiest_cu(ns, round) / speed[s], cf = busiest_cu(nf, round) / speed[f];
-    if (cs > cost[s] || cf >= cost[s]) return;
-    qs.swap(ns);
-    qf.swap(nf);
-    cost[s] = cs;
-    cost[f] = cf;
   }
 }
 
