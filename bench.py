@@ -112,11 +112,12 @@ def source_cache(ctx, L, w, kp, vp, src_indices_dev):
 
 
 def source_digest() -> str:
-    """Hash of the attention kernel sources; counter figures taken for another
-    version of the kernel are not reported."""
+    """Hash of the attention kernel sources and of the planner that places its
+    work items (which decides how often K/V cross an XCD's L2); counter figures
+    taken for another version of either are not reported."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("attn_kernel.h", "attn_pipe.h", "common.h"):
+    for f in ("attn_kernel.h", "attn_pipe.h", "common.h", "plan.h"):
         with open(os.path.join(ROOT, "paper_2607_00151_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
