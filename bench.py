@@ -210,8 +210,8 @@ def gemm_reference(n: int = 8192, reps: int = 30):
             "frac_of_bf16_peak": tflops / PEAK_BF16_TFLOPS}
 
 
-def copy_mode(nbytes: int, steps: int, warmup: int):
-    """A plain device copy (torch's copy kernel) of nbytes, the reference rate for the page
+def copy_rate(nbytes: int, steps: int = 30, warmup: int = 10) -> dict:
+    """A plain device copy (torch's copy kernel) of nbytes, the practical rate for the page
     kernels at the same byte count.  Enough source / destination pairs rotate that their
     footprint exceeds the 256 MB Infinity Cache (1 GiB or more); each copy is timed by its
     own events and the median reported."""
@@ -230,8 +230,14 @@ def copy_mode(nbytes: int, steps: int, warmup: int):
         b.record()
     torch.cuda.synchronize()
     ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
-    print(json.dumps({"mode": "copy", "bytes_read": 2 * n, "bytes_written": 2 * n, "buffer_pairs": pairs,
-                      "ms": ms, "gbs": 4 * n / (ms * 1e-3) / 1e9}), flush=True)
+    del src, dst
+    gbs = 4 * n / (ms * 1e-3) / 1e9
+    return {"bytes_read": 2 * n, "bytes_written": 2 * n, "buffer_pairs": pairs, "ms": ms, "gbs": gbs,
+            "frac_of_hbm": gbs / PEAK_HBM_GBS}
+
+
+def copy_mode(nbytes: int, steps: int, warmup: int):
+    print(json.dumps({"mode": "copy", **copy_rate(nbytes, steps, warmup)}), flush=True)
 
 
 def assemble_mode(args):
@@ -686,6 +692,10 @@ def main():
         rec["roofline"]["traffic_detail"] = traffic
     if not args.no_gemm_reference:
         rec["gemm_reference"] = gemm_reference()
+        # the practical HBM rate for the page kernels: plain copies of the step's bytes and of
+        # the 32-layer splice's
+        rec["copy_reference"] = {"kind": "torch Tensor.copy_ between contiguous buffers (median of 30)",
+                                 "step_bytes": copy_rate(42 * (1 << 20)), "all_layers_bytes": copy_rate(1 << 30)}
 
     rec["config"]["launches"] = {"attn": "splice | append + attention (one launch, segment rows read from k_new/v_new)",
                                  "splice": "splice + append | attention",
