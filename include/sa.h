@@ -279,7 +279,11 @@ sa_status sa_kv_splice_alias(sa_ctx *ctx, const sa_layout *layout, int32_t batch
  * h_q_len[b] == 0 are skipped.  Arithmetic: bf16 MFMA products with fp32
  * accumulation, fp32 online softmax, probabilities rounded to bf16 before the
  * PV product.  The scale is applied to each fp32 score (with log2(e)) before
- * the exponential.  After sa_set_exact_scale(ctx, 0) the kernel instead
+ * the exponential; a row's exponent offset moves only when its max grows by
+ * more than 2^8, and the bf16 rounding of the probability of every key that
+ * was the largest of its lane's share of the row when it arrived is carried
+ * into the normaliser of the output (not into the LSE), so a dominant key's
+ * weight comes out as its exact share.  After sa_set_exact_scale(ctx, 0) the kernel instead
  * multiplies each query row by softmax_scale * log2(e) once and rounds it to
  * bf16 (faster; moves a row's scaled scores by up to
  * 2^-8 * sum_d |scale log2(e) q_d k_d| in log2 units).
@@ -399,10 +403,12 @@ sa_status sa_set_block_clock(sa_ctx *ctx, void *d_buf, int64_t max_blocks, int64
  * differ by several percent), and a launch ends with its slowest XCD.  With
  * speeds set, the planner, when it places the work items of each KV head on
  * one XCD, evens out key tiles per unit of speed across the XCDs of a launch
- * of at most two rounds of workgroups: it swaps the longest item of the XCD
- * whose busiest CU is the most loaded for the shortest item of the least
- * loaded one (every XCD keeps its number of items).  Launches of more rounds
- * are placed as without speeds.  Results are
+ * of at most two rounds of workgroups: it pairs the XCDs by speed (slowest
+ * with fastest, and so on) and, within each pair, swaps the longest item of
+ * the XCD whose busiest CU is the more loaded for the shortest item of the
+ * other (every XCD keeps its number of items; a moved item reads its KV
+ * head's K/V through the other XCD's L2).  Launches of more rounds are placed
+ * as without speeds.  Results are
  * unchanged bit for bit (a work item's arithmetic does not depend on where it
  * runs).  h_speed: host float[8], each finite and > 0 (only ratios matter),
  * e.g. the inverse of each XCD's mean workgroup time from sa_set_block_clock
