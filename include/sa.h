@@ -281,9 +281,9 @@ sa_status sa_kv_splice_alias(sa_ctx *ctx, const sa_layout *layout, int32_t batch
  * PV product.  The scale is applied to each fp32 score (with log2(e)) before
  * the exponential; a row's exponent offset moves only when its max grows by
  * more than 2^8, and the bf16 rounding of the probability of every key that
- * was the largest of its lane's share of the row when it arrived is carried
- * into the normaliser of the output (not into the LSE), so a dominant key's
- * weight comes out as its exact share.  After sa_set_exact_scale(ctx, 0) the kernel instead
+ * was its row's largest when it arrived is carried into the normaliser of the
+ * output (not into the LSE), so a dominant key's weight comes out as its
+ * exact share.  After sa_set_exact_scale(ctx, 0) the kernel instead
  * multiplies each query row by softmax_scale * log2(e) once and rounds it to
  * bf16 (faster; moves a row's scaled scores by up to
  * 2^-8 * sum_d |scale log2(e) q_d k_d| in log2 units).
