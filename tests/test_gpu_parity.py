@@ -295,6 +295,48 @@ def test_large_and_tiny_softmax_scales(ctx, scale, std):
     check_lse(w, lse.cpu().numpy(), ref_lse)
 
 
+def _bf16_bits(x):
+    """bf16 bits of float values that bf16 holds exactly."""
+    b = np.asarray(x, dtype=np.float32).view(np.uint32)
+    assert ((b & 0xFFFF) == 0).all()
+    return (b >> 16).astype(np.uint16)
+
+
+def test_dominant_key_weight_is_exact(ctx):
+    """The default path's normaliser carries the bf16 rounding of each row's record key.
+    Every query row is e_0; key 0 scores 0 (it sets the row's offset in the first tile),
+    key 100 (second tile) scores 39.25 * scale * log2 e = 5.005 above it (no rescale, under
+    2^8), every other key about -30, and all V rows are one vector of entries in [1.5, 2).
+    Key 100's probability 2^5.005 = 32.11 is packed to bf16 as 32.0; with numerator and
+    denominator carrying the same value every output row is exactly the V row, bit for
+    bit -- an fp32 denominator alone would scale it by 33.0 / 33.11 (over half an ulp)."""
+    w = build("dominant", 41, 8, 2, 128, 16, [200, 0], [8, 5])
+    G = w.num_q_heads // w.num_kv_heads
+    rng = np.random.default_rng(41)
+    q = np.zeros((int(w.q_indptr[-1]), w.num_q_heads, 128), dtype=np.float32)
+    q[:, :, 0] = 1.0
+    k = np.zeros((int(w.kv_indptr[-1]), w.num_kv_heads, 128), dtype=np.float32)
+    k[:, :, 0] = -235.0
+    vrow = (rng.choice([-1.0, 1.0], size=128) * (1.5 + rng.integers(0, 64, size=128) / 128.0)).astype(np.float32)
+    v = np.broadcast_to(vrow, (int(w.kv_indptr[-1]), w.num_kv_heads, 128)).copy()
+    s0 = int(w.kv_indptr[0])
+    k[s0 + 0, :, 0] = 0.0
+    k[s0 + 100, :, 0] = 39.25
+    w.q, w.k, w.v = _bf16_bits(q), _bf16_bits(k), _bf16_bits(v)
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    o, lse = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+    sa.sa_sync_check(ctx)
+    got = host_u16(o)
+    n0 = int(w.qlen[0])
+    assert np.array_equal(got[:n0], np.broadcast_to(_bf16_bits(vrow), (n0, w.num_q_heads, 128)))
+    # against the oracle too (the second sequence, no prefix, is plain causal attention)
+    ref, ref_lse, _ = oracle_all(w)
+    compare(got, ref, MAX_TOL, MEAN_TOL)
+    check_lse(w, lse.cpu().numpy(), ref_lse)
+    assert G == 4
+
+
 @pytest.fixture(scope="module")
 def ctx_folded():
     """A context in the fast mode that folds the scale into the bf16 query rows."""
