@@ -23,7 +23,13 @@ from HIP events recorded on that stream around every call in a second pass of
 K steps (`ms_per_step_instrumented` is that pass's step time); the attention
 kernel's time comes from a pair of events the library binds to the kernel
 launch itself (sa_set_kernel_events), the time rocprofv3's kernel trace
-reports; the page kernels of the step are timed the same way.
+reports; the page kernels of the step are timed the same way.  The timed
+steps plan the attention with the XCD speeds the run measures on its own
+launches (sa_set_xcd_weights); `attn.without_xcd_weights` is the same kernel
+placed without them.  Context measured in the same run: torch's bf16 GEMM
+(`gemm_reference`, the practical MFMA rate) and plain device copies of the
+step's and the 32-layer splice's bytes (`copy_reference`, the practical HBM
+rate).
 """
 from __future__ import annotations
 
