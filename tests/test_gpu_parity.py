@@ -746,6 +746,43 @@ def test_random_mixed_attention(ctx, k):
     check_lse(w, lse.cpu().numpy(), ref_lse)
 
 
+@pytest.mark.parametrize("k", range(6))
+def test_random_large_batches(ctx, k):
+    """Seeded larger batches: up to 24 sequences over prefixes up to 20000 tokens, 40% decode
+    rows, G up to 16, page 16 or 32, half of them planned under random XCD speeds -- the
+    planner's multi-round, pairing, split and weighting paths on shapes no fixed case has.
+    Sampled rows (first and last token of every sequence in all heads, 8 random ones per
+    sequence) and their LSE against the oracle."""
+    r = np.random.default_rng(50000 + k)
+    B = int(r.integers(1, 25))
+    Hkv = int(r.choice([1, 2, 4, 8]))
+    G = int(r.choice([1, 2, 4, 8, 16]))
+    while Hkv * G > 64:
+        G //= 2
+    P = int(r.choice([16, 32]))
+    pre = [int(x) for x in r.integers(0, 20001, B)]
+    ql = [1 if r.random() < 0.4 else int(r.integers(1, 3001)) for _ in range(B)]
+    weighted = r.random() < 0.5
+    print(f"random large {k}: B {B} Hq {Hkv * G} Hkv {Hkv} P {P} sum pre {sum(pre)} sum q {sum(ql)} "
+          f"weighted {weighted}", flush=True)
+    w = build(f"large{k}", 50000 + k, Hkv * G, Hkv, 128, P, pre, ql)
+    L = layout_of(w)
+    kp, vp, ip, ix = build_cache(w)
+    try:
+        if weighted:
+            sa.sa_set_xcd_weights(ctx, 0.9 + 0.2 * r.random(8))
+        o, lse = attention(ctx, w, L, dev_u16(w.q), kp, vp, ip, ix)
+        sa.sa_sync_check(ctx)
+    finally:
+        sa.sa_set_xcd_weights(ctx, None)
+    toks, heads = sample_rows(w, 8, seed=k)
+    ref, ref_lse, _ = oracle.attention_rows(w.q, w.k, w.v, w.q_indptr, w.kv_indptr, w.num_q_heads,
+                                            w.num_kv_heads, w.scale, toks, heads)
+    mx, mean = compare(host_u16(o)[toks, heads], ref, MAX_TOL, MEAN_TOL)
+    print(f"  {len(toks)} rows, max {mx:.3e} mean {mean:.3e}", flush=True)
+    check_lse(w, lse.cpu().numpy()[toks, heads], ref_lse, toks, heads)
+
+
 def test_block_clock_records(ctx):
     """sa_set_block_clock: one record per workgroup, start <= end, the item's sequence and
     q_len, and the same output bits as without it; decode rows and prefill rows mixed."""
