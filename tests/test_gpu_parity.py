@@ -677,6 +677,58 @@ def test_splice_and_append_in_one_launch(ctx, name, layers, layer):
     compare(host_u16(o), ref, MAX_TOL, MEAN_TOL)
     check_lse(w, lse.cpu().numpy(), ref_lse)
 
+@pytest.mark.parametrize("k", range(4))
+def test_random_page_batches(ctx, k):
+    """Seeded larger page batches: up to 16 sequences over prefixes up to 8000 tokens, a fifth
+    of them with no new tokens, 1-4 layers with the append in a random one, the splice and
+    append in one launch or as two calls -- both pools, every layer and slot, bit for bit
+    against the oracle's splice then append."""
+    r = np.random.default_rng(60000 + k)
+    B = int(r.integers(1, 17))
+    Hkv = int(r.choice([1, 2, 4, 8]))
+    P = int(r.choice([16, 32]))
+    pre = [int(x) for x in r.integers(0, 8001, B)]
+    ql = [int(x) if r.random() < 0.8 else 0 for x in r.integers(1, 2001, B)]
+    layers = int(r.integers(1, 5))
+    layer = int(r.integers(0, layers))
+    fused = bool(r.random() < 0.5)
+    print(f"random pages {k}: B {B} Hkv {Hkv} P {P} layers {layers} append layer {layer} fused {fused}",
+          flush=True)
+    w = build(f"pages{k}", 60000 + k, Hkv, Hkv, 128, P, pre, ql, assemble=True)
+    a = w.asm
+    L = layout_of(w, num_layers=layers)
+    kp, vp, sip, sid, fresh = build_source_cache(w, num_layers=layers)
+    want_k, want_v = host_u16(kp).copy(), host_u16(vp).copy()
+    dip = torch.zeros(w.batch + 1, dtype=torch.int32, device="cuda")
+    did = torch.full((len(a.fresh),), -1, dtype=torch.int32, device="cuda")
+    if fused:
+        kept = sa.sa_kv_assemble_append(ctx, L, kp, vp, kp, vp, a.src_len, a.keep_indptr, a.keep_spans,
+                                        a.reserve, sip, sid, fresh, dip, did, layer, dev_u16(w.k_seg()),
+                                        dev_u16(w.v_seg()), w.qlen)
+    else:
+        kept = sa.sa_kv_assemble(ctx, L, kp, vp, kp, vp, a.src_len, a.keep_indptr, a.keep_spans,
+                                 a.reserve, sip, sid, fresh, dip, did)
+        sa.sa_kv_append(ctx, L, layer, kp, vp, dev_u16(w.k_seg()), dev_u16(w.v_seg()), kept, w.qlen,
+                        dip, did)
+    sa.sa_sync_check(ctx)
+    res = opages.assemble(a.src_len, a.src_indptr, a.src_indices, a.keep_indptr, a.keep_spans,
+                          a.reserve, a.fresh, w.page_size)
+    assert np.array_equal(kept, res["dst_len"])
+    assert np.array_equal(dip.cpu().numpy(), res["dst_indptr"])
+    assert np.array_equal(did.cpu().numpy()[: res["dst_indptr"][-1]], res["dst_indices"])
+    sl, ro = opages.append_destinations(res["dst_len"], w.qlen, res["dst_indptr"], res["dst_indices"],
+                                        w.page_size)
+    src = np.asarray(res["copy_src"], dtype=np.int64)
+    dst = np.asarray(res["copy_dst"], dtype=np.int64)
+    for want, seg in ((want_k, w.k_seg()), (want_v, w.v_seg())):
+        for lay in range(layers):
+            for s_, d_ in zip(src, dst):
+                want[lay, d_] = want[lay, s_]
+        opages.apply_append(want[layer], seg, sl, ro)
+    assert np.array_equal(host_u16(kp), want_k)
+    assert np.array_equal(host_u16(vp), want_v)
+
+
 def random_case(k):
     """Seeded small workload k: 1-5 sequences, prefixes 0..700 (partial pages included),
     segments 1..300, 1-4 KV heads with G in {1, 2, 4, 8}, page 16 or 32; case 12 has no
